@@ -1,0 +1,207 @@
+"""Benchmark of the InfiniPot-V compression pass on one MI355X.
+
+One step = one whole pass (TaR + VaN scores, keep-set selection, in-place
+compaction) over every (stream, layer, KV head) slice of a synthetic cache,
+through the C ABI's ipv_compress_timed. Each step compresses its own replica
+of the cache, all resident in HBM before the timed region, so nothing is
+restored inside it; a 1 GiB write evicts the caches before warm-up and before
+timing. Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 7b-class-28L]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import synth  # noqa: E402
+from synth import workloads as W  # noqa: E402
+
+METRIC = "compression-pass latency (us) + achieved HBM GB/s (% of peak), 1 MI355X"
+PEAK_HBM_GBPS = 8000.0
+STEP_NAMES = ("recent_table", "score_sweep", "pool", "select", "compact")
+
+
+class Hip:
+    """The few HIP runtime calls the benchmark makes itself (events)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        if self.lib.hipEventCreate(ctypes.byref(e)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return e.value
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        if self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+
+def pct(xs, q):
+    xs = sorted(xs)
+    return xs[min(len(xs) - 1, int(round(q * (len(xs) - 1))))]
+
+
+def make_cache(w: W.Workload):
+    sts = [synth.fresh_cache(w.seeds[s], w.layers, w.kv_heads, w.capacity, w.head_dim, w.grid_h, w.grid_w,
+                             w.n_tokens, w.dtype, w.rho_specs[s], w.value_sigma) for s in range(w.streams)]
+    st = lambda a: np.ascontiguousarray(np.stack([getattr(s, a) for s in sts]))
+    return st("K"), st("V"), st("frame_idx"), st("patch_idx")
+
+
+def cpu_baseline(w, K, V, fr, pa, alpha, seconds):
+    """The CPU oracle on the same workload, on this host's cores."""
+    import oracle
+    times = []
+    t_end = time.perf_counter() + seconds
+    while not times or (time.perf_counter() < t_end and len(times) < 50):
+        Kc, Vc, fc, pc = K.copy(), V.copy(), fr.copy(), pa.copy()
+        t = time.perf_counter()
+        oracle.compress_inplace(Kc, Vc, fc, pc, w.n_tokens, w.budget, alpha, w.recent_frames, w.grid_h, w.grid_w,
+                                w.cv_tau)
+        times.append(time.perf_counter() - t)
+    t = statistics.median(times)
+    return {"value": round(w.algorithmic_bytes() / t / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
+            "kind": "oracle", "latency_us": round(t * 1e6, 1),
+            "sample": "whole %s pass, median of %d runs" % (w.name, len(times))}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=W.SEVEN_B.name)
+    ap.add_argument("--alpha", type=float, default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the pass shards by (stream, layer, KV head) with no communication, "
+              "so only --gpus 1 is supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2506_15745_amd import ipv
+
+    w = W.BY_NAME[args.workload]
+    alpha = w.alphas[0] if args.alpha is None else args.alpha
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    hip = Hip()
+
+    K, V, fr, pa = make_cache(w)
+    kind = torch.bfloat16 if w.dtype == synth.BF16 else torch.float32
+    to_dev = lambda a, bf=False: (torch.from_numpy(a).view(kind) if bf else torch.from_numpy(a)).to(dev)
+    pristine = (to_dev(K, True), to_dev(V, True), to_dev(fr), to_dev(pa))
+    reps = args.warmup + args.steps
+    replicas = [tuple(t.clone() for t in pristine) for _ in range(reps)]
+    comp = ipv.Compressor(pristine[0], w.grid_h, w.grid_w, w.budget)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+
+    # copy ceiling: a plain device-to-device copy of the K and V bytes
+    kv_bytes = 2 * pristine[0].numel() * pristine[0].element_size()
+    src = torch.empty(kv_bytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * kv_bytes * 10 / (time.perf_counter() - t) / 1e9
+    del src, dst
+
+    events = [[hip.event() for _ in range(6)] for _ in range(reps)]
+    ev_structs = [ipv.Events(*e) for e in events]
+
+    def step(i):
+        Kd, Vd, fd, pd = replicas[i]
+        ipv.ipv_compress_timed(Kd, Vd, fd, pd, w.n_tokens, w.budget, alpha, w.recent_frames, w.cv_tau, comp.tar,
+                               comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w, ev_structs[i])
+
+    flush.fill_(1.0)
+    for i in range(args.warmup):
+        step(i)
+    flush.fill_(2.0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, reps):
+        step(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    errors = comp.device_errors()
+
+    timed = range(args.warmup, reps)
+    pass_us = [hip.elapsed_ms(events[i][0], events[i][5]) * 1e3 for i in timed]
+    step_us = {name: statistics.mean(hip.elapsed_ms(events[i][k], events[i][k + 1]) * 1e3 for i in timed)
+               for k, name in enumerate(STEP_NAMES)}
+
+    ms_per_step = wall / args.steps * 1e3
+    algo = w.algorithmic_bytes()
+    value = algo / (ms_per_step * 1e-3) / 1e9
+    B, L, H = w.streams, w.layers, w.kv_heads
+    row = w.head_dim * w.elem_bytes
+    n_recent = min(w.n_tokens, w.recent_frames * w.p)
+    if w.n_tokens % w.p:
+        n_recent = (w.recent_frames - 1) * w.p + w.n_tokens % w.p
+    algo_by_step = {"recent_table": B * L * H * n_recent * row,
+                    "score_sweep": B * L * H * (2 * w.n_tokens - n_recent) * row,
+                    "compact": B * L * H * 4 * w.budget * row}
+    dom = max(("score_sweep", "compact"), key=lambda k: step_us[k])
+    achieved = algo_by_step[dom] / (step_us[dom] * 1e-6) / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == synth.BF16 else "f32",
+        "data": "synthetic (seeded AR(1) keys, log-normal-scaled values)",
+        "config": {"workload": w.name, "streams": B, "layers": L, "kv_heads": H, "head_dim": w.head_dim,
+                   "tokens_per_frame": w.p, "n_tokens": w.n_tokens, "budget": w.budget,
+                   "recent_frames": w.recent_frames, "alpha": alpha, "parallelism": "single GPU"},
+        "latency_us": {"wall_mean": round(ms_per_step * 1e3, 2), "p50": round(pct(pass_us, 0.5), 2),
+                       "p99": round(pct(pass_us, 0.99), 2)},
+        "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
+        "tokens_per_s": round(B * w.n_tokens / (ms_per_step * 1e-3), 1),
+        "rows_per_s": round(B * L * H * w.n_tokens / (ms_per_step * 1e-3), 1),
+        "algorithmic_bytes": algo,
+        "step_us_mean": {k: round(v, 2) for k, v in step_us.items()},
+        "copy_ceiling_GBps": round(copy_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None},
+        "device_errors": errors,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, K, V, fr, pa, alpha, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

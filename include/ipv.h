@@ -1,0 +1,186 @@
+/*
+ * ipv.h -- C ABI of the InfiniPot-V KV-cache compression pass for AMD MI355X
+ * (gfx950). InfiniPot-V: "Memory-Constrained KV Cache Compression for
+ * Streaming Video Understanding" (arXiv 2506.15745).
+ *
+ * When a streaming video model's KV cache reaches its memory cap |M|, the pass
+ * shrinks every (stream, layer, KV head) slice to a budget of C rows:
+ *
+ *   ipv_tar_scores   Temporal-axis Redundancy score of every past row
+ *                    (Sec. 3.1, TaR equation)
+ *   ipv_van_scores   Value-Norm score of every row, optionally average-pooled
+ *                    with a layer-adaptive window (Sec. 3.2; Algorithm 2)
+ *   ipv_select       keep set: recent window + TaR picks + VaN picks
+ *                    (Algorithm 1 steps (3)-(5); Sec. 3.3)
+ *   ipv_compact      in-place, order-preserving gather of the kept rows
+ *                    (Sec. 3.1; Algorithm 1 step (5))
+ *   ipv_compress     the four steps above, in order, on one stream
+ *
+ * ---------------------------------------------------------------- layouts
+ * A cache holds B streams x L layers x H KV heads; each (b, l, h) "slice" has
+ * a row capacity S of which rows [0, n) are valid (n = n_tokens, the same for
+ * every slice of a call). All row-major:
+ *   K, V        [B, L, H, S, D] elements of `dtype` (bf16 or fp32), device
+ *   frame_idx   [B, L, H, S] int32, device: frame id of each row
+ *   patch_idx   [B, L, H, S] int32, device: patch position in [0, grid_h*grid_w)
+ *   tar, van    [B, L, H, S] fp32, device (only rows [0, n) are written)
+ *   keep_idx    [B, L, H, C] int32, device, strictly ascending row indices
+ *   pool_size   [B, L] int32, device (pooling window chosen per layer)
+ * Frame ids must not decrease along the rows of a slice, and a frame holds
+ * each patch position at most once. This holds for a cache that appends whole
+ * frames and is only ever compacted by this library (compaction is stable).
+ * The recent window is every row whose frame id is >= F - r + 1, where F is
+ * the frame id of row n-1 (a partial last frame counts as a frame).
+ *
+ * Pointer alignment: K, V, tar, van, frame_idx, patch_idx, keep_idx 16 bytes;
+ * the workspace 256 bytes.
+ *
+ * ---------------------------------------------------------------- ownership
+ * The caller allocates and owns every buffer, including the workspace
+ * (size from ipv_workspace_bytes). The library allocates no device memory,
+ * keeps no state between calls and is thread-safe for distinct buffers.
+ * `stream` is a hipStream_t (NULL: the default stream). Every call only
+ * enqueues work on `stream` and returns; results are visible after the
+ * stream is synchronised.
+ *
+ * ---------------------------------------------------------------- errors
+ * Host-checkable argument errors return a non-zero ipv_status before
+ * anything is enqueued and leave every buffer untouched. Problems that only
+ * the device can see (metadata breaking the invariants above, a keep index
+ * outside [j, n), a NaN score) set bits in the workspace's device error word
+ * (IPV_DEV_*); the kernels stay in bounds, skip the offending rows and carry
+ * on. Read the word with ipv_read_device_errors, reset it with
+ * ipv_clear_device_errors. IPV_ERR_HIP means a launch failed (a stream error
+ * is also reported by the next HIP call on that stream).
+ */
+#ifndef IPV_H
+#define IPV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  IPV_OK = 0,
+  IPV_ERR_NULL = 1,        /* a required pointer is NULL */
+  IPV_ERR_ALIGN = 2,       /* a pointer breaks the alignment rules above */
+  IPV_ERR_SHAPE = 3,       /* bad B/L/H/D/S/grid, n outside [1, S], or a size the kernels do not cover */
+  IPV_ERR_DTYPE = 4,       /* dtype is neither IPV_BF16 nor IPV_F32 */
+  IPV_ERR_BUDGET = 5,      /* budget outside [min(n, r*p), n] */
+  IPV_ERR_ARG = 6,         /* alpha outside [0, 1], recent_frames < 1, bad cv_tau */
+  IPV_ERR_WORKSPACE = 7,   /* workspace missing or smaller than ipv_workspace_bytes */
+  IPV_ERR_HIP = 8          /* the HIP runtime reported an error */
+} ipv_status;
+
+typedef enum { IPV_BF16 = 0, IPV_F32 = 1 } ipv_dtype;
+
+/* Device error word bits (accumulated with atomic OR until cleared). */
+enum {
+  IPV_DEV_BAD_PATCH = 1u,      /* patch_idx outside [0, p): the row scored 0 / was left out of pooling */
+  IPV_DEV_BAD_FRAMES = 2u,     /* frame ids decrease, or a (frame, patch) pair repeats in the window */
+  IPV_DEV_RECENT_OVER = 4u,    /* recent window larger than the budget: keep_idx set to 0..C-1 */
+  IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n): row j was not moved */
+  IPV_DEV_NAN = 16u            /* a candidate score is NaN: its rank is unspecified */
+};
+
+typedef struct {
+  int32_t streams;   /* B >= 1 */
+  int32_t layers;    /* L >= 1 */
+  int32_t kv_heads;  /* H >= 1 */
+  int32_t head_dim;  /* D: 32, 64, 128 or 256 */
+  int32_t capacity;  /* S: row stride of a slice, S >= n */
+  int32_t grid_h;    /* patch grid of a frame: p = grid_h * grid_w tokens per frame */
+  int32_t grid_w;
+  int32_t dtype;     /* ipv_dtype of K and V */
+} ipv_shape;
+
+/* Bytes of device workspace every call on this shape needs (>= 256). */
+ipv_status ipv_workspace_bytes(const ipv_shape* shape, size_t* bytes);
+
+/*
+ * TaR score (Sec. 3.1, TaR equation). For a past row x at patch position q:
+ *   tar[x] = -(1/r_q) * sum over the r_q recent rows y at position q of cos(K[x], K[y])
+ * with cos = 0 when either key is zero, and tar[x] = 0 when r_q = 0 (a
+ * position missing from a partial recent frame). Recent rows get 0. -0.0 is
+ * written as +0.0. fp32 accumulation. Requires 1 <= r <= 256 and r * p <= 65536.
+ */
+ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* frame_idx,
+                          const int32_t* patch_idx, int32_t n_tokens, int32_t recent_frames, float* tar,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * VaN score (Sec. 3.2): van[x] = ||V[x]||_2 for every valid row, fp32.
+ * With cv_tau (host pointer to three doubles tau1 <= tau2 <= tau3) the scores
+ * are pooled per layer (Algorithm 2): CV = std/mean over all heads and valid
+ * rows of the layer (population std), window k = 7 if CV < tau1, 5 if
+ * CV < tau2, 3 if CV < tau3, else 1; each row's score becomes the mean over
+ * the rows of its own frame and slice whose grid cell lies in the k x k window
+ * around its cell (stride 1, cells outside the grid or absent are skipped).
+ * cv_tau NULL: no pooling. pool_size (device, [B, L], may be NULL) receives k.
+ */
+ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* frame_idx,
+                          const int32_t* patch_idx, int32_t n_tokens, const double* cv_tau, float* van,
+                          int32_t* pool_size, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Keep set of `budget` = C rows per slice (Algorithm 1 steps (3)-(5); Sec. 3.3):
+ *   b_T = max(0, floor(alpha * C) - |R|),  b_V = C - |R| - b_T   (floor taken in double)
+ *   T = the b_T past rows with the highest tar, V = the b_V past rows outside T
+ *   with the highest van; equal scores go to the lower row index, -0.0 == +0.0.
+ *   keep_idx = R u T u V in ascending order.
+ * Requires min(n, r*p) <= C <= n and n <= 65536.
+ */
+ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van, const int32_t* frame_idx,
+                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, int32_t* keep_idx,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * In-place compaction (Sec. 3.1; Algorithm 1 step (5)): for j < C, row j of
+ * K, V, frame_idx and patch_idx becomes a bit copy of row keep_idx[j]. Needs
+ * keep_idx[j] in [j, n) (true for any ascending keep set); rows [C, S) are
+ * left unspecified and free for new frames. The caller then sets n = C.
+ * ws may be NULL (device errors are then not reported).
+ */
+ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                       int32_t n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* The whole pass: ipv_tar_scores, ipv_van_scores, ipv_select, ipv_compact. */
+ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                        const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/*
+ * ipv_compress with per-kernel timing: each non-NULL entry of `at` is a
+ * hipEvent_t (created by the caller) recorded on `stream` at a step boundary:
+ *   at[0] before the recent-key table   at[1] before the TaR/VaN sweep
+ *   at[2] before pooling                at[3] before selection
+ *   at[4] before compaction             at[5] after compaction
+ * Elapsed time between consecutive events is that step's device time.
+ */
+typedef struct {
+  void* at[6];
+} ipv_events;
+
+ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                              int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                              const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
+                              size_t ws_bytes, void* stream, const ipv_events* events);
+
+/* Reset the workspace's device error word (a small kernel on `stream`). */
+ipv_status ipv_clear_device_errors(void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronise `stream` and copy the device error word to *flags (host). */
+ipv_status ipv_read_device_errors(const void* ws, size_t ws_bytes, void* stream, uint32_t* flags);
+
+/* Static description of a status code. */
+const char* ipv_status_str(ipv_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* IPV_H */

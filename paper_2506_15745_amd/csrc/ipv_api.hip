@@ -1,0 +1,367 @@
+// C ABI of the compression pass: argument validation, workspace layout and
+// kernel launches. Every check that the host can make happens before the
+// first launch, so a rejected call enqueues nothing and touches no buffer.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/ipv.h"
+#include "ipv_compact.hpp"
+#include "ipv_scores.hpp"
+#include "ipv_select.hpp"
+
+using namespace ipv;
+
+#define IPV_TRY(x)               \
+  do {                           \
+    const ipv_status _s = (x);   \
+    if (_s != IPV_OK) return _s; \
+  } while (0)
+
+namespace {
+
+constexpr int32_t kMaxRows = kSelThreads * 64;  // select keeps 64 row flags per thread
+constexpr int64_t kMaxWindowRows = 65536;        // r * p: recent rows scanned per table block
+constexpr int32_t kMaxRecentFrames = 256;
+
+struct Dims {
+  int64_t B, L, H, S, D, p, slices;
+  int32_t gh, gw, dtype;
+  int64_t elem;  // bytes per element
+};
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+ipv_status check_shape(const ipv_shape* s, Dims* d) {
+  if (!s) return IPV_ERR_NULL;
+  if (s->dtype != IPV_BF16 && s->dtype != IPV_F32) return IPV_ERR_DTYPE;
+  if (s->streams < 1 || s->layers < 1 || s->kv_heads < 1 || s->capacity < 1 || s->grid_h < 1 || s->grid_w < 1)
+    return IPV_ERR_SHAPE;
+  if (s->head_dim != 32 && s->head_dim != 64 && s->head_dim != 128 && s->head_dim != 256) return IPV_ERR_SHAPE;
+  const int64_t p = (int64_t)s->grid_h * s->grid_w;
+  if (p > kPoolCells) return IPV_ERR_SHAPE;
+  d->B = s->streams;
+  d->L = s->layers;
+  d->H = s->kv_heads;
+  d->S = s->capacity;
+  d->D = s->head_dim;
+  d->p = p;
+  d->slices = d->B * d->L * d->H;
+  d->gh = s->grid_h;
+  d->gw = s->grid_w;
+  d->dtype = s->dtype;
+  d->elem = s->dtype == IPV_BF16 ? 2 : 4;
+  if (d->slices > (int64_t)INT32_MAX / 8) return IPV_ERR_SHAPE;
+  return IPV_OK;
+}
+
+ipv_status check_rows(const Dims& d, int32_t n) {
+  if (n < 1 || n > d.S || n > kMaxRows) return IPV_ERR_SHAPE;
+  return IPV_OK;
+}
+
+ipv_status check_recent(const Dims& d, int32_t r) {
+  if (r < 1 || r > kMaxRecentFrames) return IPV_ERR_ARG;
+  if ((int64_t)r * d.p > kMaxWindowRows) return IPV_ERR_ARG;
+  return IPV_OK;
+}
+
+ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
+  const int64_t window = std::min<int64_t>(n, (int64_t)r * d.p);
+  if (budget < window || budget > n || budget < 1) return IPV_ERR_BUDGET;
+  return IPV_OK;
+}
+
+// ------------------------------------------------------------ workspace layout
+// [0, 256)                 device error word (uint32) + padding
+// table  slices * p * D    fp32 m_q vectors of the recent window
+// pool   B * L             int32 pooling window per (stream, layer)
+size_t table_offset() { return kWsHeader; }
+size_t table_bytes(const Dims& d) { return (size_t)(d.slices * d.p * d.D) * sizeof(float); }
+size_t pool_offset(const Dims& d) { return (table_offset() + table_bytes(d) + 255) / 256 * 256; }
+size_t ws_total(const Dims& d) { return (pool_offset(d) + (size_t)(d.B * d.L) * sizeof(int32_t) + 255) / 256 * 256; }
+
+ipv_status check_ws(const Dims& d, const void* ws, size_t ws_bytes) {
+  if (!ws) return IPV_ERR_WORKSPACE;
+  if (!aligned(ws, 256)) return IPV_ERR_ALIGN;
+  if (ws_bytes < ws_total(d)) return IPV_ERR_WORKSPACE;
+  return IPV_OK;
+}
+
+uint32_t* err_word(void* ws) { return reinterpret_cast<uint32_t*>(ws); }
+float* ws_table(void* ws) { return reinterpret_cast<float*>(static_cast<char*>(ws) + table_offset()); }
+int32_t* ws_pool(void* ws, const Dims& d) {
+  return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pool_offset(d));
+}
+
+ipv_status launched() { return hipGetLastError() == hipSuccess ? IPV_OK : IPV_ERR_HIP; }
+
+uint32_t pad8(uint32_t x) { return (x + 7u) / 8u * 8u; }
+
+// ------------------------------------------------------------ launchers
+ipv_status no_mark() { return IPV_OK; }
+
+// between(): runs after the recent-key table is enqueued, before the sweep
+template <typename T, int D, typename Between>
+ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
+                      int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between) {
+  const bool do_tar = K != nullptr, do_van = V != nullptr;
+  if (do_tar) {
+    constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
+    const int32_t blocks = (int32_t)((d.p + GROUPS - 1) / GROUPS);
+    const size_t lds = (size_t)GROUPS * r * sizeof(int32_t);
+    k_recent_table<T, D><<<dim3((uint32_t)(d.slices * blocks)), dim3(256), lds, st>>>(
+        static_cast<const T*>(K), fr, pa, d.S, n, r, (int32_t)d.p, blocks, ws_table(ws), err_word(ws));
+  }
+  IPV_TRY(between());
+  using C = SweepCfg<T, D>;
+  const int32_t tiles = (n + C::TILE - 1) / C::TILE;
+  const uint32_t work = (uint32_t)(d.slices * tiles);
+  const dim3 grid(pad8(work)), block(256);
+  const T* k = static_cast<const T*>(K);
+  const T* v = static_cast<const T*>(V);
+  if (do_tar && do_van)
+    k_score_sweep<T, D, true, true><<<grid, block, 0, st>>>(k, v, fr, pa, d.S, n, r, (int32_t)d.p, ws_table(ws), tar,
+                                                            van, err_word(ws), tiles, work);
+  else if (do_tar)
+    k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, fr, pa, d.S, n, r, (int32_t)d.p, ws_table(ws),
+                                                             tar, van, err_word(ws), tiles, work);
+  else
+    k_score_sweep<T, D, false, true><<<grid, block, 0, st>>>(k, v, fr, pa, d.S, n, r, (int32_t)d.p, ws_table(ws),
+                                                             tar, van, err_word(ws), tiles, work);
+  return launched();
+}
+
+template <typename Between = ipv_status (*)()>
+ipv_status scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
+                  int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between = no_mark) {
+#define IPV_SCORES(T, DD) \
+  if (d.D == DD) return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between);
+  if (d.dtype == IPV_BF16) {
+    IPV_SCORES(uint16_t, 32) IPV_SCORES(uint16_t, 64) IPV_SCORES(uint16_t, 128) IPV_SCORES(uint16_t, 256)
+  } else {
+    IPV_SCORES(float, 32) IPV_SCORES(float, 64) IPV_SCORES(float, 128) IPV_SCORES(float, 256)
+  }
+#undef IPV_SCORES
+  return IPV_ERR_SHAPE;
+}
+
+ipv_status pool_d(const Dims& d, const double* tau, float* van, const int32_t* fr, const int32_t* pa, int32_t n,
+                  int32_t* pool_out, void* ws, hipStream_t st) {
+  k_pool_cv<<<dim3((uint32_t)(d.B * d.L)), dim3(256), 0, st>>>(van, d.S, n, (int32_t)d.H, tau[0], tau[1], tau[2],
+                                                               ws_pool(ws, d), pool_out);
+  k_pool_apply<<<dim3((uint32_t)d.slices), dim3(256), 0, st>>>(van, fr, pa, d.S, n, (int32_t)d.H, d.gh, d.gw,
+                                                               ws_pool(ws, d));
+  return launched();
+}
+
+__global__ void k_fill_i32(int32_t* p, int64_t count, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) p[i] = v;
+}
+
+template <int RPT>
+ipv_status run_select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
+                      int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st) {
+  k_select<RPT><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget, tar_total, r,
+                                                                        keep, err);
+  return launched();
+}
+
+ipv_status select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
+                  int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st) {
+  const int32_t rpt = (n + kSelThreads - 1) / kSelThreads;
+  if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
+  if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
+  if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
+  if (rpt <= 32) return run_select<32>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
+  return run_select<64>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
+}
+
+template <int RB>
+ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
+                       int32_t budget, uint32_t* err, hipStream_t st) {
+  const uint32_t grid = (uint32_t)(d.slices * 2 * CompactCfg<RB>::NCB);
+  k_compact<RB><<<dim3(grid), dim3(256), 0, st>>>(static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n,
+                                                  budget, keep, err);
+  return launched();
+}
+
+ipv_status compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
+                   int32_t budget, uint32_t* err, hipStream_t st) {
+  switch (d.D * d.elem) {
+    case 64: return run_compact<64>(d, K, V, fr, pa, n, keep, budget, err, st);
+    case 128: return run_compact<128>(d, K, V, fr, pa, n, keep, budget, err, st);
+    case 256: return run_compact<256>(d, K, V, fr, pa, n, keep, budget, err, st);
+    case 512: return run_compact<512>(d, K, V, fr, pa, n, keep, budget, err, st);
+    case 1024: return run_compact<1024>(d, K, V, fr, pa, n, keep, budget, err, st);
+  }
+  return IPV_ERR_SHAPE;
+}
+
+int32_t floor_share(double alpha, int32_t budget) { return (int32_t)std::floor(alpha * (double)budget); }
+
+ipv_status check_tau(const double* tau) {
+  if (!tau) return IPV_OK;
+  for (int i = 0; i < 3; ++i)
+    if (!std::isfinite(tau[i])) return IPV_ERR_ARG;
+  if (!(tau[0] <= tau[1] && tau[1] <= tau[2])) return IPV_ERR_ARG;
+  return IPV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ipv_status ipv_workspace_bytes(const ipv_shape* shape, size_t* bytes) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!bytes) return IPV_ERR_NULL;
+  *bytes = ws_total(d);
+  return IPV_OK;
+}
+
+ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* frame_idx, const int32_t* patch_idx,
+                          int32_t n_tokens, int32_t recent_frames, float* tar, void* ws, size_t ws_bytes,
+                          void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!K || !frame_idx || !patch_idx || !tar) return IPV_ERR_NULL;
+  if (!aligned(K, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) || !aligned(tar, 16)) return IPV_ERR_ALIGN;
+  IPV_TRY(check_rows(d, n_tokens));
+  IPV_TRY(check_recent(d, recent_frames));
+  IPV_TRY(check_ws(d, ws, ws_bytes));
+  return scores(d, K, nullptr, frame_idx, patch_idx, n_tokens, recent_frames, tar, nullptr, ws,
+                static_cast<hipStream_t>(stream));
+}
+
+ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* frame_idx, const int32_t* patch_idx,
+                          int32_t n_tokens, const double* cv_tau, float* van, int32_t* pool_size, void* ws,
+                          size_t ws_bytes, void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!V || !frame_idx || !patch_idx || !van) return IPV_ERR_NULL;
+  if (!aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) || !aligned(van, 16)) return IPV_ERR_ALIGN;
+  if (pool_size && !aligned(pool_size, 4)) return IPV_ERR_ALIGN;
+  IPV_TRY(check_rows(d, n_tokens));
+  IPV_TRY(check_tau(cv_tau));
+  IPV_TRY(check_ws(d, ws, ws_bytes));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  IPV_TRY(scores(d, nullptr, V, frame_idx, patch_idx, n_tokens, 1, nullptr, van, ws, st));
+  if (cv_tau) return pool_d(d, cv_tau, van, frame_idx, patch_idx, n_tokens, pool_size, ws, st);
+  if (pool_size) {
+    const int64_t cnt = d.B * d.L;
+    k_fill_i32<<<dim3((uint32_t)((cnt + 255) / 256)), dim3(256), 0, st>>>(pool_size, cnt, 1);
+    return launched();
+  }
+  return IPV_OK;
+}
+
+ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van, const int32_t* frame_idx,
+                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, int32_t* keep_idx,
+                      void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!tar || !van || !frame_idx || !keep_idx) return IPV_ERR_NULL;
+  if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(frame_idx, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
+  IPV_TRY(check_rows(d, n_tokens));
+  IPV_TRY(check_recent(d, recent_frames));
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
+  IPV_TRY(check_budget(d, n_tokens, budget, recent_frames));
+  IPV_TRY(check_ws(d, ws, ws_bytes));
+  return select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
+                err_word(ws), static_cast<hipStream_t>(stream));
+}
+
+ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                       int32_t n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
+                       void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!K || !V || !frame_idx || !patch_idx || !keep_idx) return IPV_ERR_NULL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
+      !aligned(keep_idx, 16))
+    return IPV_ERR_ALIGN;
+  IPV_TRY(check_rows(d, n_tokens));
+  if (budget < 1 || budget > n_tokens) return IPV_ERR_BUDGET;
+  if (ws) IPV_TRY(check_ws(d, ws, ws_bytes));
+  return compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws ? err_word(ws) : nullptr,
+                 static_cast<hipStream_t>(stream));
+}
+
+ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                              int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                              const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
+                              size_t ws_bytes, void* stream, const ipv_events* events) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!K || !V || !frame_idx || !patch_idx || !tar || !van || !keep_idx) return IPV_ERR_NULL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
+      !aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16))
+    return IPV_ERR_ALIGN;
+  IPV_TRY(check_rows(d, n_tokens));
+  IPV_TRY(check_recent(d, recent_frames));
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
+  IPV_TRY(check_budget(d, n_tokens, budget, recent_frames));
+  IPV_TRY(check_tau(cv_tau));
+  IPV_TRY(check_ws(d, ws, ws_bytes));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  auto mark = [&](int i) -> ipv_status {
+    if (!events || !events->at[i]) return IPV_OK;
+    return hipEventRecord(static_cast<hipEvent_t>(events->at[i]), st) == hipSuccess ? IPV_OK : IPV_ERR_HIP;
+  };
+  IPV_TRY(mark(0));
+  IPV_TRY(scores(d, K, V, frame_idx, patch_idx, n_tokens, recent_frames, tar, van, ws, st,
+                 [&]() { return mark(1); }));
+  IPV_TRY(mark(2));
+  if (cv_tau) IPV_TRY(pool_d(d, cv_tau, van, frame_idx, patch_idx, n_tokens, nullptr, ws, st));
+  IPV_TRY(mark(3));
+  IPV_TRY(select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
+                 err_word(ws), st));
+  IPV_TRY(mark(4));
+  IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, err_word(ws), st));
+  return mark(5);
+}
+
+ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, const double* cv_tau,
+                        float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream) {
+  return ipv_compress_timed(shape, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar,
+                            van, keep_idx, ws, ws_bytes, stream, nullptr);
+}
+
+ipv_status ipv_clear_device_errors(void* ws, size_t ws_bytes, void* stream) {
+  if (!ws) return IPV_ERR_NULL;
+  if (!aligned(ws, 256)) return IPV_ERR_ALIGN;
+  if (ws_bytes < kWsHeader) return IPV_ERR_WORKSPACE;
+  k_fill_i32<<<dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream)>>>(static_cast<int32_t*>(ws), 1, 0);
+  return launched();
+}
+
+ipv_status ipv_read_device_errors(const void* ws, size_t ws_bytes, void* stream, uint32_t* flags) {
+  if (!ws || !flags) return IPV_ERR_NULL;
+  if (!aligned(ws, 256)) return IPV_ERR_ALIGN;
+  if (ws_bytes < kWsHeader) return IPV_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipMemcpyAsync(flags, ws, sizeof(uint32_t), hipMemcpyDeviceToHost, st) != hipSuccess) return IPV_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return IPV_ERR_HIP;
+  return IPV_OK;
+}
+
+const char* ipv_status_str(ipv_status s) {
+  switch (s) {
+    case IPV_OK: return "ok";
+    case IPV_ERR_NULL: return "a required pointer is NULL";
+    case IPV_ERR_ALIGN: return "a pointer is not aligned as required";
+    case IPV_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case IPV_ERR_DTYPE: return "unsupported dtype";
+    case IPV_ERR_BUDGET: return "budget outside [min(n, r*p), n]";
+    case IPV_ERR_ARG: return "invalid argument (alpha, recent_frames or cv_tau)";
+    case IPV_ERR_WORKSPACE: return "workspace missing or too small";
+    case IPV_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,289 @@
+// Scoring kernels of the compression pass: the recent-key table, the fused
+// TaR + VaN row sweep, and the layer-adaptive VaN pooling.
+//
+// TaR (Sec. 3.1, TaR equation) averages cos(K[x], K[y]) over the recent rows y
+// at x's patch position. Cosine is linear in the unit vectors, so
+//   -(1/r_q) sum_y cos(K[x], K[y]) = -(K[x]/|K[x]|) . m_q,
+//   m_q = (1/r_q) sum_y K[y]/|K[y]|   (zero keys contribute the zero vector),
+// and the sweep reads each past key once against a per-slice table of m_q
+// (fp32, p x D) that the first kernel builds from the recent window.
+#pragma once
+
+#include "ipv_device.hpp"
+
+namespace ipv {
+
+// ---------------------------------------------------------------- recent-key table
+// One workgroup per (slice, block of patch positions). Each lane group of
+// LPR lanes owns one patch position q and sums the unit recent keys at q in
+// frame order (deterministic), then scales by 1/r_q. Positions with no recent
+// key get m_q = 0, which makes their TaR score 0.
+// LDS: slot[g * r + (frame - first_recent_frame)] = row of that key, or -1.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
+                                                      const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                      int32_t r, int32_t p, int32_t blocks_per_slice,
+                                                      float* __restrict__ table, uint32_t* err) {
+  constexpr int EPL = Lane<T>::EPL;
+  constexpr int LPR = D / EPL;
+  constexpr int GROUPS = 256 / LPR;
+  extern __shared__ int32_t slot[];
+
+  const int tid = threadIdx.x;
+  const int64_t slice = blockIdx.x / blocks_per_slice;
+  const int32_t q0 = (blockIdx.x % blocks_per_slice) * GROUPS;
+  const int32_t q1 = min(p, q0 + GROUPS);
+  const int64_t base = slice * S;
+  const int64_t thr = (int64_t)frame_idx[base + n - 1] - r + 1;
+
+  for (int i = tid; i < GROUPS * r; i += 256) slot[i] = -1;
+  __syncthreads();
+  // A recent frame holds at most p rows, so the window lies in the last r*p rows.
+  const int64_t t0 = max((int64_t)0, (int64_t)n - (int64_t)r * p);
+  for (int64_t t = t0 + tid; t < n; t += 256) {
+    const int32_t f = frame_idx[base + t];
+    if (f < thr) continue;
+    const int32_t q = patch_idx[base + t];
+    if (q < 0 || q >= p) {
+      raise_error(err, 1u);
+      continue;
+    }
+    if (q < q0 || q >= q1) continue;
+    const int64_t fo = (int64_t)f - thr;
+    if (fo >= r) {  // a frame id above the last row's: ids decrease somewhere
+      raise_error(err, 2u);
+      continue;
+    }
+    if (atomicExch(&slot[(q - q0) * r + fo], (int32_t)t) != -1) raise_error(err, 2u);
+  }
+  __syncthreads();
+
+  const int g = tid / LPR, lane = tid % LPR;
+  const int32_t q = q0 + g;
+  float acc[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+  int cnt = 0;
+  if (q < q1) {
+    for (int j = 0; j < r; ++j) {
+      const int32_t y = slot[g * r + j];
+      if (y < 0) continue;
+      ++cnt;
+      float f[EPL];
+      Lane<T>::decode(load16(K + (base + y) * D + lane * EPL), f);
+      float ss = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
+      ss = group_sum<LPR>(ss);
+      const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) acc[i] += f[i] * inv;
+    }
+    const float scale = cnt ? 1.f / (float)cnt : 0.f;
+    float* out = table + ((int64_t)slice * p + q) * D + lane * EPL;
+#pragma unroll
+    for (int i = 0; i < EPL; i += 4)
+      *reinterpret_cast<float4*>(out + i) = make_float4(acc[i] * scale, acc[i + 1] * scale, acc[i + 2] * scale,
+                                                        acc[i + 3] * scale);
+  }
+}
+
+// ---------------------------------------------------------------- fused TaR + VaN sweep
+// Each row is read by a group of LPR lanes, 16 bytes per lane; a workgroup of
+// 256 threads covers GROUPS consecutive rows per step and U steps per tile,
+// issuing all of its K/V loads before any arithmetic. Workgroups are
+// renumbered so the tiles of one slice share an XCD (and the slice's m table
+// stays in that XCD's L2).
+template <typename T, int D>
+struct SweepCfg {
+  static constexpr int EPL = Lane<T>::EPL;
+  static constexpr int LPR = D / EPL;
+  static constexpr int GROUPS = 256 / LPR;
+  static constexpr int U = 4;
+  static constexpr int TILE = GROUPS * U;
+};
+
+template <typename T, int D, bool TAR, bool VAN>
+__global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, const T* __restrict__ V,
+                                                     const int32_t* __restrict__ frame_idx,
+                                                     const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                     int32_t r, int32_t p, const float* __restrict__ table,
+                                                     float* __restrict__ tar, float* __restrict__ van,
+                                                     uint32_t* err, int32_t tiles_per_slice, uint32_t n_work) {
+  using C = SweepCfg<T, D>;
+  constexpr int EPL = C::EPL, LPR = C::LPR, GROUPS = C::GROUPS, U = C::U;
+  const uint32_t logical = xcd_logical_id(blockIdx.x, gridDim.x);
+  if (logical >= n_work) return;
+  const int64_t slice = logical / tiles_per_slice;
+  const int64_t row0 = (int64_t)(logical % tiles_per_slice) * C::TILE;
+  const int64_t base = slice * S;
+  const int tid = threadIdx.x, g = tid / LPR, lane = tid % LPR;
+
+  int64_t thr = 0;
+  if (TAR) thr = (int64_t)frame_idx[base + n - 1] - r + 1;
+
+  Raw16 kr[U], vr[U];
+  int32_t fq[U], pq[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t x = row0 + u * GROUPS + g;
+    fq[u] = 0;
+    pq[u] = -1;
+    if (x < n) {
+      if (TAR) {
+        fq[u] = frame_idx[base + x];
+        pq[u] = patch_idx[base + x];
+        kr[u] = load16(K + (base + x) * D + lane * EPL);
+      }
+      if (VAN) vr[u] = load16(V + (base + x) * D + lane * EPL);
+    }
+  }
+  if (VAN) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t x = row0 + u * GROUPS + g;
+      float f[EPL];
+      float ss = 0.f;
+      if (x < n) {
+        Lane<T>::decode(vr[u], f);
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
+      }
+      ss = group_sum<LPR>(ss);
+      if (x < n && lane == 0) van[base + x] = sqrtf(ss);
+    }
+  }
+  if (TAR) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t x = row0 + u * GROUPS + g;
+      const bool past = x < n && (int64_t)fq[u] < thr;
+      const bool ok = past && pq[u] >= 0 && pq[u] < p;
+      if (past && !ok && lane == 0) raise_error(err, 1u);
+      float dot = 0.f, kk = 0.f;
+      if (ok) {
+        float f[EPL];
+        Lane<T>::decode(kr[u], f);
+        const float* m = table + ((int64_t)slice * p + pq[u]) * D + lane * EPL;
+#pragma unroll
+        for (int i = 0; i < EPL; i += 4) {
+          const float4 mv = *reinterpret_cast<const float4*>(m + i);
+          dot += f[i] * mv.x + f[i + 1] * mv.y + f[i + 2] * mv.z + f[i + 3] * mv.w;
+          kk += f[i] * f[i] + f[i + 1] * f[i + 1] + f[i + 2] * f[i + 2] + f[i + 3] * f[i + 3];
+        }
+      }
+      dot = group_sum<LPR>(dot);
+      kk = group_sum<LPR>(kk);
+      if (x < n && lane == 0) {
+        float s = kk > 0.f ? -(dot / sqrtf(kk)) : 0.f;
+        if (s == 0.f) s = 0.f;  // -0.0 -> +0.0
+        tar[base + x] = past ? s : 0.f;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- adaptive pooling
+// Per (stream, layer): CV of all H * n VaN values in fp64, two passes (mean,
+// then squared deviations), fixed-order reduction; window k from the
+// thresholds. One workgroup per (stream, layer).
+__global__ __launch_bounds__(256) void k_pool_cv(const float* __restrict__ van, int64_t S, int32_t n, int32_t H,
+                                                 double tau1, double tau2, double tau3,
+                                                 int32_t* __restrict__ pool_ws, int32_t* __restrict__ pool_out) {
+  __shared__ double red[256];
+  const int tid = threadIdx.x;
+  const int64_t bl = blockIdx.x;
+  const int64_t count = (int64_t)H * n;
+  double s = 0.0;
+  for (int64_t i = tid; i < count; i += 256) s += (double)van[(bl * H + i / n) * S + i % n];
+  red[tid] = s;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (tid < w) red[tid] += red[tid + w];
+    __syncthreads();
+  }
+  const double mean = red[0] / (double)count;
+  __syncthreads();
+  double v = 0.0;
+  for (int64_t i = tid; i < count; i += 256) {
+    const double d = (double)van[(bl * H + i / n) * S + i % n] - mean;
+    v += d * d;
+  }
+  red[tid] = v;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (tid < w) red[tid] += red[tid + w];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const double sd = sqrt(red[0] / (double)count);
+    const double cv = mean == 0.0 ? 0.0 : sd / mean;
+    const int32_t k = cv < tau1 ? 7 : cv < tau2 ? 5 : cv < tau3 ? 3 : 1;
+    pool_ws[bl] = k;
+    if (pool_out) pool_out[bl] = k;
+  }
+}
+
+// One workgroup per slice. Frames are handled FR at a time: their raw VaN
+// values are scattered into an LDS grid (absent cells hold -1), then every
+// row of those frames averages the present cells of its k x k window and
+// overwrites its own score. Rows of later frames still hold raw values. Each
+// round starts at the smallest frame id not yet covered, so the loop runs at
+// most once per present frame whatever the ids are.
+constexpr int kPoolCells = 8192;
+
+__global__ __launch_bounds__(256) void k_pool_apply(float* __restrict__ van, const int32_t* __restrict__ frame_idx,
+                                                    const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                    int32_t H, int32_t grid_h, int32_t grid_w,
+                                                    const int32_t* __restrict__ pool_ws) {
+  __shared__ float cell[kPoolCells];
+  __shared__ int32_t next_frame;
+  const int tid = threadIdx.x;
+  const int64_t slice = blockIdx.x;
+  const int32_t k = pool_ws[slice / H];
+  if (k == 1) return;
+  const int32_t half = k / 2, p = grid_h * grid_w, FR = kPoolCells / p;
+  const int64_t base = slice * S;
+  int64_t lower = INT64_MIN;
+  for (;;) {
+    if (tid == 0) next_frame = INT32_MAX;
+    for (int i = tid; i < FR * p; i += 256) cell[i] = -1.f;
+    __syncthreads();
+    int32_t mine = INT32_MAX;
+    for (int64_t x = tid; x < n; x += 256) {
+      const int32_t f = frame_idx[base + x];
+      if ((int64_t)f >= lower && f < mine) mine = f;
+    }
+    atomicMin(&next_frame, mine);
+    __syncthreads();
+    const int64_t fb = next_frame;
+    if (fb == INT32_MAX) break;
+    for (int64_t x = tid; x < n; x += 256) {
+      const int64_t fo = (int64_t)frame_idx[base + x] - fb;
+      const int32_t q = patch_idx[base + x];
+      if (fo >= 0 && fo < FR && q >= 0 && q < p) cell[fo * p + q] = van[base + x];
+    }
+    __syncthreads();
+    for (int64_t x = tid; x < n; x += 256) {
+      const int64_t fo = (int64_t)frame_idx[base + x] - fb;
+      const int32_t q = patch_idx[base + x];
+      if (fo < 0 || fo >= FR || q < 0 || q >= p) continue;
+      const int32_t ci = q / grid_w, cj = q % grid_w;
+      float sum = 0.f;
+      int cnt = 0;
+      for (int32_t i = max(0, ci - half); i <= min(grid_h - 1, ci + half); ++i)
+        for (int32_t j = max(0, cj - half); j <= min(grid_w - 1, cj + half); ++j) {
+          const float c = cell[fo * p + i * grid_w + j];
+          if (c >= 0.f) {
+            sum += c;
+            ++cnt;
+          }
+        }
+      van[base + x] = sum / (float)cnt;
+    }
+    lower = fb + FR;
+    __syncthreads();
+  }
+}
+
+}  // namespace ipv

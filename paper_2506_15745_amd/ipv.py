@@ -1,0 +1,224 @@
+"""Python binding of ``libipv.so`` (ctypes; argument marshalling only).
+
+Every function here passes device pointers of torch tensors, sizes and the
+current HIP stream to the C ABI declared in ``include/ipv.h``; all of the
+pass's work runs in the library's HIP kernels. Importing works anywhere, but
+the first call loads ``libipv.so`` and raises :class:`IpvError` when it has
+not been built -- there is no fallback implementation.
+
+Tensor layouts (all contiguous, on the same GPU):
+  K, V        [B, L, H, S, D]  torch.bfloat16 or torch.float32
+  frame_idx   [B, L, H, S]     torch.int32
+  patch_idx   [B, L, H, S]     torch.int32
+  tar, van    [B, L, H, S]     torch.float32
+  keep_idx    [B, L, H, C]     torch.int32
+  pool_size   [B, L]           torch.int32
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libipv.so")
+
+OK, ERR_NULL, ERR_ALIGN, ERR_SHAPE, ERR_DTYPE, ERR_BUDGET, ERR_ARG, ERR_WORKSPACE, ERR_HIP = range(9)
+BF16, F32 = 0, 1
+DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN = 1, 2, 4, 8, 16
+
+EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
+           "ipv_compress", "ipv_compress_timed", "ipv_clear_device_errors", "ipv_read_device_errors",
+           "ipv_status_str")
+
+
+class IpvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (what, status_str(status), status))
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("streams", "layers", "kv_heads", "head_dim", "capacity", "grid_h", "grid_w", "dtype")]
+
+
+class Events(ctypes.Structure):
+    """hipEvent_t handles recorded at the pass's step boundaries (see ipv.h)."""
+    _fields_ = [("at", ctypes.c_void_p * 6)]
+
+    def __init__(self, *handles):
+        super().__init__()
+        for i, h in enumerate(handles):
+            self.at[i] = h
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises IpvError if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise IpvError(ERR_HIP, "libipv.so is not built (run paper_2506_15745_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_double, ctypes.c_size_t
+        sp = ctypes.POINTER(Shape)
+        L.ipv_workspace_bytes.argtypes = [sp, ctypes.POINTER(ctypes.c_size_t)]
+        L.ipv_tar_scores.argtypes = [sp, vp, vp, vp, i32, i32, vp, vp, sz, vp]
+        L.ipv_van_scores.argtypes = [sp, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
+        L.ipv_select.argtypes = [sp, vp, vp, vp, i32, i32, f64, i32, vp, vp, sz, vp]
+        L.ipv_compact.argtypes = [sp, vp, vp, vp, vp, i32, vp, i32, vp, sz, vp]
+        L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, vp, vp, vp, vp, vp, sz, vp,
+                                         ctypes.POINTER(Events)]
+        L.ipv_clear_device_errors.argtypes = [vp, sz, vp]
+        L.ipv_read_device_errors.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
+        L.ipv_status_str.argtypes = [ctypes.c_int]
+        L.ipv_status_str.restype = ctypes.c_char_p
+        for name in EXPORTS[:-1]:
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_str(status: int) -> str:
+    if _lib is None and not os.path.exists(LIB_PATH):
+        return "status %d" % status
+    return lib().ipv_status_str(status).decode()
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise IpvError(rc, what)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise IpvError(ERR_DTYPE, "K/V dtype %s" % t.dtype)
+
+
+def shape_of(K: torch.Tensor, grid_h: int, grid_w: int) -> Shape:
+    if K.dim() != 5:
+        raise IpvError(ERR_SHAPE, "K must be [B, L, H, S, D]")
+    B, L, H, S, D = K.shape
+    return Shape(B, L, H, D, S, grid_h, grid_w, _dtype_code(K))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise IpvError(ERR_SHAPE, "tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def workspace_bytes(shape: Shape) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().ipv_workspace_bytes(ctypes.byref(shape), ctypes.byref(out)), "ipv_workspace_bytes")
+    return out.value
+
+
+def alloc_workspace(shape: Shape, device) -> torch.Tensor:
+    """A zeroed workspace tensor (uint8) for calls on `shape`."""
+    return torch.zeros(workspace_bytes(shape), dtype=torch.uint8, device=device)
+
+
+def ipv_tar_scores(K, frame_idx, patch_idx, n_tokens, recent_frames, tar, ws, grid_h, grid_w, stream=None):
+    s = shape_of(K, grid_h, grid_w)
+    _check(lib().ipv_tar_scores(ctypes.byref(s), _ptr(K), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                                recent_frames, _ptr(tar), _ptr(ws), ws.numel(), _stream(stream)), "ipv_tar_scores")
+
+
+def ipv_van_scores(V, frame_idx, patch_idx, n_tokens, cv_tau, van, pool_size, ws, grid_h, grid_w, stream=None):
+    s = shape_of(V, grid_h, grid_w)
+    tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
+    _check(lib().ipv_van_scores(ctypes.byref(s), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                                None if tau is None else ctypes.addressof(tau), _ptr(van), _ptr(pool_size),
+                                _ptr(ws), ws.numel(), _stream(stream)), "ipv_van_scores")
+
+
+def ipv_select(tar, van, frame_idx, n_tokens, budget, alpha, recent_frames, keep_idx, ws, grid_h, grid_w,
+               head_dim=128, dtype=BF16, stream=None):
+    """The select step needs only the slice geometry: (B, L, H, S) from the
+    score tensors and the patch grid; head_dim/dtype only size the workspace."""
+    B, L, H, S = tar.shape
+    s = Shape(B, L, H, head_dim, S, grid_h, grid_w, dtype)
+    _check(lib().ipv_select(ctypes.byref(s), _ptr(tar), _ptr(van), _ptr(frame_idx), n_tokens, budget,
+                            float(alpha), recent_frames, _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream)),
+           "ipv_select")
+
+
+def ipv_compact(K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, grid_h, grid_w, stream=None):
+    s = shape_of(K, grid_h, grid_w)
+    _check(lib().ipv_compact(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                             _ptr(keep_idx), budget, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)),
+           "ipv_compact")
+
+
+def ipv_compress(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van, keep_idx,
+                 ws, grid_h, grid_w, stream=None):
+    s = shape_of(K, grid_h, grid_w)
+    tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
+    _check(lib().ipv_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                              budget, float(alpha), recent_frames, None if tau is None else ctypes.addressof(tau),
+                              _ptr(tar), _ptr(van), _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream)),
+           "ipv_compress")
+
+
+def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van,
+                       keep_idx, ws, grid_h, grid_w, events: Events, stream=None):
+    s = shape_of(K, grid_h, grid_w)
+    tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
+    _check(lib().ipv_compress_timed(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                                    budget, float(alpha), recent_frames,
+                                    None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
+                                    _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(events)),
+           "ipv_compress_timed")
+
+
+def ipv_clear_device_errors(ws, stream=None):
+    _check(lib().ipv_clear_device_errors(_ptr(ws), ws.numel(), _stream(stream)), "ipv_clear_device_errors")
+
+
+def ipv_read_device_errors(ws, stream=None) -> int:
+    out = ctypes.c_uint32(0)
+    _check(lib().ipv_read_device_errors(_ptr(ws), ws.numel(), _stream(stream), ctypes.byref(out)),
+           "ipv_read_device_errors")
+    return out.value
+
+
+class Compressor:
+    """Buffers for repeated passes over caches of one shape.
+
+    Holds the score, keep-index and workspace tensors so a pass allocates
+    nothing; ``compress`` runs the whole pass on the current stream.
+    """
+
+    def __init__(self, K: torch.Tensor, grid_h: int, grid_w: int, budget: int):
+        self.grid_h, self.grid_w, self.budget = grid_h, grid_w, budget
+        self.shape = shape_of(K, grid_h, grid_w)
+        B, L, H, S, D = K.shape
+        dev = K.device
+        self.tar = torch.zeros((B, L, H, S), dtype=torch.float32, device=dev)
+        self.van = torch.zeros((B, L, H, S), dtype=torch.float32, device=dev)
+        self.keep_idx = torch.zeros((B, L, H, budget), dtype=torch.int32, device=dev)
+        self.ws = alloc_workspace(self.shape, dev)
+
+    def compress(self, K, V, frame_idx, patch_idx, n_tokens, alpha, recent_frames, cv_tau=None, stream=None):
+        ipv_compress(K, V, frame_idx, patch_idx, n_tokens, self.budget, alpha, recent_frames, cv_tau, self.tar,
+                     self.van, self.keep_idx, self.ws, self.grid_h, self.grid_w, stream)
+
+    def device_errors(self) -> int:
+        return ipv_read_device_errors(self.ws)

@@ -1,0 +1,120 @@
+"""GPU-vs-oracle comparison helpers (test infrastructure).
+
+Acceptance rules:
+  * scores: |gpu - oracle| <= 1e-3 * max(1, |oracle|) for TaR, <= 1e-3 * |oracle|
+    (+1e-6 absolute) for VaN, against the oracle's fp64 values;
+  * keep sets: identical per slice, except rows whose oracle score lies within
+    1e-3 * max(1, |cut|) of the stage's cut score (reported, and each such flip
+    may displace one more row at the VaN boundary);
+  * compaction: bit-exact against the oracle's gather with the GPU's keep_idx.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2506_15745_amd import ipv
+
+TAR_TOL = 1e-3
+VAN_TOL = 1e-3
+
+
+def to_device(a: np.ndarray, kind: str = "raw", device="cuda:0") -> torch.Tensor:
+    """numpy -> device tensor; kind 'bf16' reinterprets uint16 bits as bfloat16."""
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if kind == "bf16":
+        t = t.view(torch.bfloat16)
+    return t.to(device)
+
+
+def to_host(t: torch.Tensor) -> np.ndarray:
+    if t.dtype == torch.bfloat16:
+        t = t.view(torch.int16)
+        return t.cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+@dataclass
+class GpuPass:
+    tar: np.ndarray
+    van: np.ndarray
+    keep: np.ndarray
+    K: np.ndarray
+    V: np.ndarray
+    frame_idx: np.ndarray
+    patch_idx: np.ndarray
+    errors: int
+    pool_size: np.ndarray | None = None
+
+
+def gpu_compress(K, V, fr, pa, n, budget, alpha, r, gh, gw, cv_tau=None, steps=False) -> GpuPass:
+    """Run the pass on cuda:0 through the C ABI. steps=True calls the four
+    entry points one by one instead of ipv_compress."""
+    kind = "bf16" if K.dtype == np.uint16 else "raw"
+    Kd, Vd = to_device(K, kind), to_device(V, kind)
+    frd, pad = to_device(fr), to_device(pa)
+    B, L, H, S, D = K.shape
+    tar = torch.zeros((B, L, H, S), dtype=torch.float32, device="cuda:0")
+    van = torch.zeros_like(tar)
+    keep = torch.zeros((B, L, H, budget), dtype=torch.int32, device="cuda:0")
+    shape = ipv.shape_of(Kd, gh, gw)
+    ws = ipv.alloc_workspace(shape, "cuda:0")
+    pool = torch.zeros((B, L), dtype=torch.int32, device="cuda:0")
+    if steps:
+        ipv.ipv_tar_scores(Kd, frd, pad, n, r, tar, ws, gh, gw)
+        ipv.ipv_van_scores(Vd, frd, pad, n, cv_tau, van, pool, ws, gh, gw)
+        ipv.ipv_select(tar, van, frd, n, budget, alpha, r, keep, ws, gh, gw, head_dim=D, dtype=shape.dtype)
+        ipv.ipv_compact(Kd, Vd, frd, pad, n, keep, budget, ws, gh, gw)
+    else:
+        ipv.ipv_compress(Kd, Vd, frd, pad, n, budget, alpha, r, cv_tau, tar, van, keep, ws, gh, gw)
+    torch.cuda.synchronize()
+    errors = ipv.ipv_read_device_errors(ws)
+    return GpuPass(to_host(tar), to_host(van), to_host(keep), to_host(Kd), to_host(Vd), to_host(frd),
+                   to_host(pad), errors, to_host(pool) if steps else None)
+
+
+def check_scores(g_tar, g_van, o_tar, o_van, n, name=""):
+    gt, gv = g_tar[..., :n].astype(np.float64), g_van[..., :n].astype(np.float64)
+    ot, ov = o_tar[..., :n], o_van[..., :n]
+    et = np.abs(gt - ot) / np.maximum(1.0, np.abs(ot))
+    ev = np.abs(gv - ov) / np.maximum(np.abs(ov), 1e-3)
+    assert et.max() <= TAR_TOL, "%s TaR rel err %.3g" % (name, et.max())
+    assert np.all(np.abs(gv - ov) <= VAN_TOL * np.abs(ov) + 1e-6), "%s VaN rel err %.3g" % (name, ev.max())
+    return float(et.max()), float(ev.max())
+
+
+def check_keep(g_keep, sel: oracle.Selection, o_tar, o_van):
+    """Keep-set rule; returns (near-threshold rows, unexplained rows) totals."""
+    near_total = 0
+    for idx in np.ndindex(g_keep.shape[:3]):
+        g, o = set(g_keep[idx].tolist()), set(sel.keep_idx[idx].tolist())
+        if g == o:
+            continue
+        diff = g ^ o
+        ct, cv = float(sel.cut_tar[idx]), float(sel.cut_van[idx])
+        near_t = {x for x in diff if not math.isnan(ct) and abs(o_tar[idx][x] - ct) <= 1e-3 * max(1, abs(ct))}
+        near_v = {x for x in diff if not math.isnan(cv) and abs(o_van[idx][x] - cv) <= 1e-3 * max(1, abs(cv))}
+        rest = diff - near_t - near_v
+        assert len(rest) <= len(near_t), "slice %s: rows %s differ beyond the near-threshold rule" % (idx, sorted(rest))
+        near_total += len(near_t | near_v)
+    return near_total
+
+
+def check_ascending(keep, n):
+    assert np.all(np.diff(keep, axis=-1) > 0), "keep_idx not strictly ascending"
+    assert keep.min() >= 0 and keep.max() < n
+
+
+def oracle_gather_equal(K0, V0, fr0, pa0, n, keep, got: GpuPass):
+    """Compaction parity: the oracle's gather of the ORIGINAL cache with the
+    GPU's keep_idx must equal the GPU's compacted rows [0, C) bit for bit."""
+    C = keep.shape[-1]
+    Ko, Vo, fo, po = oracle.compact(K0, V0, fr0, pa0, n, np.ascontiguousarray(keep))
+    assert np.array_equal(got.K[..., :C, :].view(np.uint8), Ko[..., :C, :].view(np.uint8)), "K compaction differs"
+    assert np.array_equal(got.V[..., :C, :].view(np.uint8), Vo[..., :C, :].view(np.uint8)), "V compaction differs"
+    assert np.array_equal(got.frame_idx[..., :C], fo[..., :C]), "frame_idx compaction differs"
+    assert np.array_equal(got.patch_idx[..., :C], po[..., :C]), "patch_idx compaction differs"

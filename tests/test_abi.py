@@ -1,0 +1,141 @@
+"""The C ABI on the host: the library loads, exports every function the
+header declares, and rejects bad arguments before anything is launched.
+
+Every call here carries at least one argument the host checks reject, so no
+kernel is ever enqueued (these tests run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_15745_amd import ipv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    with open(os.path.join(ROOT, "include", "ipv.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ipv_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    names = declared_functions()
+    assert "ipv_compress" in names and len(names) >= 10
+    L = ipv.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(ipv.EXPORTS)
+
+
+def test_status_strings():
+    for s in range(9):
+        assert ipv.status_str(s) and ipv.status_str(s) != "unknown status"
+    assert ipv.lib().ipv_status_str(1234) == b"unknown status"
+
+
+SEVEN_B = dict(streams=1, layers=28, kv_heads=4, head_dim=128, capacity=6272, grid_h=14, grid_w=14, dtype=0)
+FAKE = 0x10000  # a 256-aligned non-null address; never dereferenced because another argument is rejected
+
+
+def shape(**kw):
+    d = dict(SEVEN_B)
+    d.update(kw)
+    return ipv.Shape(*[d[k] for k in ("streams", "layers", "kv_heads", "head_dim", "capacity", "grid_h", "grid_w",
+                                      "dtype")])
+
+
+def ws_bytes(s):
+    return ipv.workspace_bytes(s)
+
+
+def test_workspace_size_covers_the_recent_table():
+    s = shape()
+    assert ws_bytes(s) >= 256 + 28 * 4 * 196 * 128 * 4
+    with pytest.raises(ipv.IpvError) as e:
+        ipv.workspace_bytes(shape(head_dim=96))
+    assert e.value.status == ipv.ERR_SHAPE
+    with pytest.raises(ipv.IpvError) as e:
+        ipv.workspace_bytes(shape(dtype=7))
+    assert e.value.status == ipv.ERR_DTYPE
+
+
+def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, ws=FAKE, wsb=None, K=FAKE):
+    p = dict(K=K, V=FAKE, fr=FAKE, pa=FAKE, tar=FAKE, van=FAKE, keep=FAKE)
+    if ptrs:
+        p.update(ptrs)
+    t = None if tau is None else (ctypes.c_double * 3)(*tau)
+    wsb = wsb if wsb is not None else 0  # default: workspace too small
+    return ipv.lib().ipv_compress(ctypes.byref(s), p["K"], p["V"], p["fr"], p["pa"], n, budget, alpha, r,
+                                  None if t is None else ctypes.addressof(t), p["tar"], p["van"], p["keep"], ws,
+                                  wsb, None)
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(ptrs=dict(K=None)), ipv.ERR_NULL),
+    (dict(ptrs=dict(keep=None)), ipv.ERR_NULL),
+    (dict(ptrs=dict(V=FAKE + 8)), ipv.ERR_ALIGN),
+    (dict(ptrs=dict(tar=FAKE + 4)), ipv.ERR_ALIGN),
+    (dict(n=0), ipv.ERR_SHAPE),
+    (dict(n=6273), ipv.ERR_SHAPE),                # n > capacity
+    (dict(budget=6273), ipv.ERR_BUDGET),          # budget > n
+    (dict(budget=783), ipv.ERR_BUDGET),           # smaller than r * p
+    (dict(alpha=1.5), ipv.ERR_ARG),
+    (dict(alpha=float("nan")), ipv.ERR_ARG),
+    (dict(r=0), ipv.ERR_ARG),
+    (dict(r=257), ipv.ERR_ARG),
+    (dict(tau=(0.5, 0.3, 0.7)), ipv.ERR_ARG),
+    (dict(tau=(0.1, float("inf"), 0.7)), ipv.ERR_ARG),
+    (dict(ws=None), ipv.ERR_WORKSPACE),
+    (dict(ws=FAKE + 16), ipv.ERR_ALIGN),
+    (dict(), ipv.ERR_WORKSPACE),                  # ws_bytes = 0
+])
+def test_compress_rejects_before_launch(case, status):
+    assert call_compress(shape(), **case) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=100), ipv.ERR_SHAPE),
+    (dict(streams=0), ipv.ERR_SHAPE),
+    (dict(grid_w=0), ipv.ERR_SHAPE),
+    (dict(grid_h=100, grid_w=100), ipv.ERR_SHAPE),   # more patches than the pooling grid holds
+    (dict(dtype=3), ipv.ERR_DTYPE),
+])
+def test_bad_shapes(kw, status):
+    assert call_compress(shape(**kw), wsb=1 << 40) == status
+
+
+def test_rows_above_select_limit_rejected():
+    s = shape(capacity=70000)
+    assert call_compress(s, n=70000, budget=35000, wsb=1 << 40) == ipv.ERR_SHAPE
+
+
+def test_entry_points_validate_their_own_arguments():
+    L, s = ipv.lib(), shape()
+    big = 1 << 40
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 0, FAKE, FAKE, big, None) == ipv.ERR_ARG
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, None, FAKE, 6272, 4, FAKE, FAKE, big, None) == ipv.ERR_NULL
+    assert L.ipv_van_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, None, FAKE, FAKE + 2, FAKE, big,
+                            None) == ipv.ERR_ALIGN
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 3136, -0.1, 4, FAKE, FAKE, big,
+                        None) == ipv.ERR_ARG
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 100, 0.5, 4, FAKE, FAKE, big,
+                        None) == ipv.ERR_BUDGET
+    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE, 0, None, 0, None) == ipv.ERR_BUDGET
+    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE + 4, 10, None, 0,
+                         None) == ipv.ERR_ALIGN
+    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE, 10, FAKE, 8, None) == ipv.ERR_WORKSPACE
+    assert L.ipv_clear_device_errors(None, 256, None) == ipv.ERR_NULL
+    assert L.ipv_clear_device_errors(FAKE, 8, None) == ipv.ERR_WORKSPACE
+    out = ctypes.c_uint32()
+    assert L.ipv_read_device_errors(FAKE + 1, 256, None, ctypes.byref(out)) == ipv.ERR_ALIGN
+    assert L.ipv_workspace_bytes(None, None) == ipv.ERR_NULL
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch):
+    monkeypatch.setattr(ipv, "_lib", None)
+    monkeypatch.setattr(ipv, "LIB_PATH", "/nonexistent/libipv.so")
+    with pytest.raises(ipv.IpvError):
+        ipv.lib()
