@@ -112,7 +112,9 @@ def main():
     kind = torch.bfloat16 if w.dtype == synth.BF16 else torch.float32
     to_dev = lambda a, bf=False: (torch.from_numpy(a).view(kind) if bf else torch.from_numpy(a)).to(dev)
     pristine = (to_dev(K, True), to_dev(V, True), to_dev(fr), to_dev(pa))
-    reps = args.warmup + args.steps
+    # replicas: warm-up, the timed steps, then the per-kernel (event) steps
+    ev_steps = min(args.steps, 10)
+    reps = args.warmup + args.steps + ev_steps
     replicas = [tuple(t.clone() for t in pristine) for _ in range(reps)]
     comp = ipv.Compressor(pristine[0], w.grid_h, w.grid_w, w.budget)
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
@@ -134,10 +136,14 @@ def main():
     events = [[hip.event() for _ in range(6)] for _ in range(reps)]
     ev_structs = [ipv.Events(*e) for e in events]
 
-    def step(i):
+    def step(i, timed_kernels=False):
         Kd, Vd, fd, pd = replicas[i]
-        ipv.ipv_compress_timed(Kd, Vd, fd, pd, w.n_tokens, w.budget, alpha, w.recent_frames, w.cv_tau, comp.tar,
-                               comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w, ev_structs[i])
+        if timed_kernels:
+            ipv.ipv_compress_timed(Kd, Vd, fd, pd, w.n_tokens, w.budget, alpha, w.recent_frames, w.cv_tau,
+                                   comp.tar, comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w, ev_structs[i])
+        else:
+            ipv.ipv_compress(Kd, Vd, fd, pd, w.n_tokens, w.budget, alpha, w.recent_frames, w.cv_tau, comp.tar,
+                             comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w)
 
     flush.fill_(1.0)
     for i in range(args.warmup):
@@ -145,13 +151,18 @@ def main():
     flush.fill_(2.0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.warmup, reps):
+    for i in range(args.warmup, args.warmup + args.steps):
         step(i)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    # per-kernel breakdown on further replicas, with events between the kernels
+    flush.fill_(3.0)
+    for i in range(args.warmup + args.steps, reps):
+        step(i, timed_kernels=True)
+    torch.cuda.synchronize()
     errors = comp.device_errors()
 
-    timed = range(args.warmup, reps)
+    timed = range(args.warmup + args.steps, reps)
     pass_us = [hip.elapsed_ms(events[i][0], events[i][5]) * 1e3 for i in timed]
     step_us = {name: statistics.mean(hip.elapsed_ms(events[i][k], events[i][k + 1]) * 1e3 for i in timed)
                for k, name in enumerate(STEP_NAMES)}
@@ -186,8 +197,8 @@ def main():
         "config": {"workload": w.name, "streams": B, "layers": L, "kv_heads": H, "head_dim": w.head_dim,
                    "tokens_per_frame": w.p, "n_tokens": w.n_tokens, "budget": w.budget,
                    "recent_frames": w.recent_frames, "alpha": alpha, "parallelism": "single GPU"},
-        "latency_us": {"wall_mean": round(ms_per_step * 1e3, 2), "p50": round(pct(pass_us, 0.5), 2),
-                       "p99": round(pct(pass_us, 0.99), 2)},
+        "latency_us": {"wall_mean": round(ms_per_step * 1e3, 2), "events_p50": round(pct(pass_us, 0.5), 2),
+                       "events_p99": round(pct(pass_us, 0.99), 2)},
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
         "tokens_per_s": round(B * w.n_tokens / (ms_per_step * 1e-3), 1),
         "rows_per_s": round(B * L * H * w.n_tokens / (ms_per_step * 1e-3), 1),

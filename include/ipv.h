@@ -35,6 +35,9 @@
  * Pointer alignment: K, V, tar, van, frame_idx, patch_idx, keep_idx 16 bytes;
  * the workspace 256 bytes.
  *
+ * Workspace: ipv_workspace_bytes(shape) bytes of device memory. Calls that
+ * share a workspace must not overlap in time.
+ *
  * ---------------------------------------------------------------- ownership
  * The caller allocates and owns every buffer, including the workspace
  * (size from ipv_workspace_bytes). The library allocates no device memory,
@@ -83,7 +86,9 @@ enum {
   IPV_DEV_BAD_FRAMES = 2u,     /* frame ids decrease, or a (frame, patch) pair repeats in the window */
   IPV_DEV_RECENT_OVER = 4u,    /* recent window larger than the budget: keep_idx set to 0..C-1 */
   IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n): row j was not moved */
-  IPV_DEV_NAN = 16u            /* a candidate score is NaN: its rank is unspecified */
+  IPV_DEV_NAN = 16u,           /* a candidate score is NaN: its rank is unspecified */
+  IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired (a workspace shared by
+                                  overlapping calls); its rows were not moved */
 };
 
 typedef struct {
@@ -142,7 +147,8 @@ ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van
  * K, V, frame_idx and patch_idx becomes a bit copy of row keep_idx[j]. Needs
  * keep_idx[j] in [j, n) (true for any ascending keep set); rows [C, S) are
  * left unspecified and free for new frames. The caller then sets n = C.
- * ws may be NULL (device errors are then not reported).
+ * All chunks of all slices are copied in parallel; a chunk stores only after
+ * every earlier chunk that reads its rows has loaded them (flags in ws).
  */
 ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                        int32_t n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,

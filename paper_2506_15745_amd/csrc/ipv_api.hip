@@ -21,7 +21,7 @@ using namespace ipv;
 
 namespace {
 
-constexpr int32_t kMaxRows = kSelThreads * 64;  // select keeps 64 row flags per thread
+constexpr int32_t kMaxRows = 65536;  // select: 1024 threads x 64 row flags
 constexpr int64_t kMaxWindowRows = 65536;        // r * p: recent rows scanned per table block
 constexpr int32_t kMaxRecentFrames = 256;
 
@@ -76,11 +76,20 @@ ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
 // ------------------------------------------------------------ workspace layout
 // [0, 256)                 device error word (uint32) + padding
 // table  slices * p * D    fp32 m_q vectors of the recent window
+// first  slices            int32 first recent row of each slice
 // pool   B * L             int32 pooling window per (stream, layer)
+// flags  walks * chunks    uint32 per compaction chunk (1 once its rows are loaded)
+size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+int64_t compact_parts(const Dims& d) { return 2 * std::max<int64_t>(1, d.D * d.elem / 128) + 1; }
+int64_t max_chunks(const Dims& d) { return (d.S + kChunkRows - 1) / kChunkRows; }
 size_t table_offset() { return kWsHeader; }
 size_t table_bytes(const Dims& d) { return (size_t)(d.slices * d.p * d.D) * sizeof(float); }
-size_t pool_offset(const Dims& d) { return (table_offset() + table_bytes(d) + 255) / 256 * 256; }
-size_t ws_total(const Dims& d) { return (pool_offset(d) + (size_t)(d.B * d.L) * sizeof(int32_t) + 255) / 256 * 256; }
+size_t first_offset(const Dims& d) { return up256(table_offset() + table_bytes(d)); }
+size_t pool_offset(const Dims& d) { return up256(first_offset(d) + (size_t)d.slices * sizeof(int32_t)); }
+size_t flags_offset(const Dims& d) { return up256(pool_offset(d) + (size_t)(d.B * d.L) * sizeof(int32_t)); }
+size_t ws_total(const Dims& d) {
+  return up256(flags_offset(d) + (size_t)(d.slices * compact_parts(d) * max_chunks(d)) * sizeof(uint32_t));
+}
 
 ipv_status check_ws(const Dims& d, const void* ws, size_t ws_bytes) {
   if (!ws) return IPV_ERR_WORKSPACE;
@@ -91,6 +100,12 @@ ipv_status check_ws(const Dims& d, const void* ws, size_t ws_bytes) {
 
 uint32_t* err_word(void* ws) { return reinterpret_cast<uint32_t*>(ws); }
 float* ws_table(void* ws) { return reinterpret_cast<float*>(static_cast<char*>(ws) + table_offset()); }
+int32_t* ws_first(void* ws, const Dims& d) {
+  return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + first_offset(d));
+}
+uint32_t* ws_flags(void* ws, const Dims& d) {
+  return reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + flags_offset(d));
+}
 int32_t* ws_pool(void* ws, const Dims& d) {
   return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pool_offset(d));
 }
@@ -112,24 +127,27 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
     const int32_t blocks = (int32_t)((d.p + GROUPS - 1) / GROUPS);
     const size_t lds = (size_t)GROUPS * r * sizeof(int32_t);
     k_recent_table<T, D><<<dim3((uint32_t)(d.slices * blocks)), dim3(256), lds, st>>>(
-        static_cast<const T*>(K), fr, pa, d.S, n, r, (int32_t)d.p, blocks, ws_table(ws), err_word(ws));
+        static_cast<const T*>(K), fr, pa, d.S, n, r, (int32_t)d.p, blocks, ws_table(ws), ws_first(ws, d),
+        err_word(ws));
   }
   IPV_TRY(between());
   using C = SweepCfg<T, D>;
-  const int32_t tiles = (n + C::TILE - 1) / C::TILE;
-  const uint32_t work = (uint32_t)(d.slices * tiles);
+  const int32_t col_blocks = (int32_t)((d.p + C::GROUPS - 1) / C::GROUPS);
+  const int32_t frame_blocks = (int32_t)(((n + d.p - 1) / d.p + C::U - 1) / C::U);
+  const uint32_t work = (uint32_t)(d.slices * frame_blocks * col_blocks);
   const dim3 grid(pad8(work)), block(256);
   const T* k = static_cast<const T*>(K);
   const T* v = static_cast<const T*>(V);
+  int32_t* first = ws_first(ws, d);
   if (do_tar && do_van)
-    k_score_sweep<T, D, true, true><<<grid, block, 0, st>>>(k, v, fr, pa, d.S, n, r, (int32_t)d.p, ws_table(ws), tar,
-                                                            van, err_word(ws), tiles, work);
+    k_score_sweep<T, D, true, true><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first, tar,
+                                                            van, err_word(ws), col_blocks, frame_blocks, work);
   else if (do_tar)
-    k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, fr, pa, d.S, n, r, (int32_t)d.p, ws_table(ws),
-                                                             tar, van, err_word(ws), tiles, work);
+    k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
+                                                             tar, van, err_word(ws), col_blocks, frame_blocks, work);
   else
-    k_score_sweep<T, D, false, true><<<grid, block, 0, st>>>(k, v, fr, pa, d.S, n, r, (int32_t)d.p, ws_table(ws),
-                                                             tar, van, err_word(ws), tiles, work);
+    k_score_sweep<T, D, false, true><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
+                                                             tar, van, err_word(ws), col_blocks, frame_blocks, work);
   return launched();
 }
 
@@ -161,11 +179,15 @@ __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t v) {
   if (i < count) p[i] = v;
 }
 
+constexpr int kSelThreads = 1024;
+
 template <int RPT>
 ipv_status run_select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
                       int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st) {
-  k_select<RPT><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget, tar_total, r,
-                                                                        keep, err);
+  // 16-byte row-run loads need every slice to start 16-byte aligned
+  const int32_t vec = (d.S % 4 == 0) ? 1 : 0;
+  k_select<kSelThreads, RPT><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget,
+                                                                                      tar_total, r, vec, keep, err);
   return launched();
 }
 
@@ -181,21 +203,24 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
 
 template <int RB>
 ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
-                       int32_t budget, uint32_t* err, hipStream_t st) {
-  const uint32_t grid = (uint32_t)(d.slices * 2 * CompactCfg<RB>::NCB);
-  k_compact<RB><<<dim3(grid), dim3(256), 0, st>>>(static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n,
-                                                  budget, keep, err);
+                       int32_t budget, void* ws, hipStream_t st) {
+  const uint32_t chunks = (uint32_t)((budget + kChunkRows - 1) / kChunkRows);
+  const int64_t total = d.slices * CompactCfg<RB>::PARTS * chunks;
+  k_clear_flags<<<dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), total);
+  k_compact<RB><<<dim3((uint32_t)total), dim3(256), 0, st>>>(static_cast<char*>(K), static_cast<char*>(V), fr, pa,
+                                                             d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
+                                                             chunks);
   return launched();
 }
 
 ipv_status compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
-                   int32_t budget, uint32_t* err, hipStream_t st) {
+                   int32_t budget, void* ws, hipStream_t st) {
   switch (d.D * d.elem) {
-    case 64: return run_compact<64>(d, K, V, fr, pa, n, keep, budget, err, st);
-    case 128: return run_compact<128>(d, K, V, fr, pa, n, keep, budget, err, st);
-    case 256: return run_compact<256>(d, K, V, fr, pa, n, keep, budget, err, st);
-    case 512: return run_compact<512>(d, K, V, fr, pa, n, keep, budget, err, st);
-    case 1024: return run_compact<1024>(d, K, V, fr, pa, n, keep, budget, err, st);
+    case 64: return run_compact<64>(d, K, V, fr, pa, n, keep, budget, ws, st);
+    case 128: return run_compact<128>(d, K, V, fr, pa, n, keep, budget, ws, st);
+    case 256: return run_compact<256>(d, K, V, fr, pa, n, keep, budget, ws, st);
+    case 512: return run_compact<512>(d, K, V, fr, pa, n, keep, budget, ws, st);
+    case 1024: return run_compact<1024>(d, K, V, fr, pa, n, keep, budget, ws, st);
   }
   return IPV_ERR_SHAPE;
 }
@@ -285,9 +310,8 @@ ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_
     return IPV_ERR_ALIGN;
   IPV_TRY(check_rows(d, n_tokens));
   if (budget < 1 || budget > n_tokens) return IPV_ERR_BUDGET;
-  if (ws) IPV_TRY(check_ws(d, ws, ws_bytes));
-  return compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws ? err_word(ws) : nullptr,
-                 static_cast<hipStream_t>(stream));
+  IPV_TRY(check_ws(d, ws, ws_bytes));
+  return compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, static_cast<hipStream_t>(stream));
 }
 
 ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
@@ -320,7 +344,7 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
   IPV_TRY(select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
                  err_word(ws), st));
   IPV_TRY(mark(4));
-  IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, err_word(ws), st));
+  IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, st));
   return mark(5);
 }
 

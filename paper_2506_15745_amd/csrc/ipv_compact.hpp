@@ -1,89 +1,167 @@
 // In-place, order-preserving compaction (Sec. 3.1; Algorithm 1 step (5)):
 // row j <- row keep[j] for j < C, for K, V, frame_idx and patch_idx.
 //
-// Safety of doing it in place: keep is ascending, so keep[j] >= j. Output
-// rows are processed in chunks [j0, j0 + CH) by ONE workgroup walking its
-// chunks in order. A chunk reads rows keep[j] >= j0 and writes rows < j0 + CH;
-// every later chunk reads only rows >= j0 + CH. So once all of a chunk's
-// loads have landed (wait on the memory counter, then a workgroup barrier) its
-// stores cannot clobber anything still to be read, and the next chunk's
-// loads may be issued while those stores drain. Independent walks run per
-// (slice, tensor, column block): columns never alias across walks.
+// The rows of a slice form independent "walks": each 128-byte column block of
+// K, each of V, and the metadata pair. A walk's output rows are cut into
+// chunks of CH rows and every chunk is one workgroup, so the whole copy runs
+// in parallel. The in-place hazard: a chunk writes rows [c0, c1) that an
+// earlier chunk of the same walk may still have to read (keep[j] >= j, so a
+// chunk's sources lie at or after its own rows, never before). Hence:
+//   1. workgroups are numbered chunk-major (all walks' chunk 0, then chunk 1,
+//      ...), so every chunk a workgroup can depend on has a lower id;
+//   2. a workgroup loads its source rows into registers, waits until they
+//      have landed in every wave, and sets its chunk's "loaded" flag;
+//   3. it waits for the flags of the earlier chunks of its walk whose
+//      source range overlaps [c0, c1), then stores.
+// Workgroups are dispatched in increasing id order (round-robin over the
+// XCDs, in order within each), so the lowest unfinished workgroup is always
+// resident and every chunk it waits for has already set its flag: the
+// waits always end. A chunk's flag depends only on its own loads. The spin
+// is bounded all the same; on expiry the chunk reports IPV_DEV_WAIT_TIMEOUT
+// and does not store.
+//
+// The flags (one uint32 per chunk, in the workspace) must be zero when the
+// kernel starts; k_clear_flags (or the selection kernel) zeroes them.
 #pragma once
 
 #include "ipv_device.hpp"
 
 namespace ipv {
 
+constexpr int kChunkRows = 128;
+constexpr uint32_t kSpinLimit = 1u << 20;
+
 template <int RB>  // bytes per row
 struct CompactCfg {
-  static constexpr int CB = RB < 128 ? RB : 128;  // bytes per column block
+  static constexpr int CB = RB < 128 ? RB : 128;  // bytes per column block (one cache line)
   static constexpr int NCB = RB / CB;             // column blocks per row
   static constexpr int LPP = CB / 16;             // lanes per row piece
   static constexpr int RPS = 256 / LPP;           // rows per step
-  static constexpr int U = 8;                     // steps per chunk
-  static constexpr int CH = RPS * U;              // rows per chunk
+  static constexpr int U = kChunkRows / RPS;      // steps per chunk
+  static constexpr int PARTS = 2 * NCB + 1;       // walks per slice: K blocks, V blocks, metadata
 };
 
-// grid: slices * 2 * NCB workgroups; work w -> (slice, tensor K/V, column block)
+__device__ inline uint32_t load_flag(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline void store_flag(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Zero `count` chunk flags.
+__global__ void k_clear_flags(uint32_t* flags, int64_t count) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) flags[i] = 0u;
+}
+
+// grid: slices * PARTS * n_chunks workgroups of 256 threads, id = chunk * walks + walk
 template <int RB>
 __global__ __launch_bounds__(256) void k_compact(char* __restrict__ K, char* __restrict__ V,
                                                  int32_t* __restrict__ frame_idx, int32_t* __restrict__ patch_idx,
                                                  int64_t S, int32_t n, int32_t budget,
-                                                 const int32_t* __restrict__ keep_idx, uint32_t* err) {
+                                                 const int32_t* __restrict__ keep_idx, uint32_t* err,
+                                                 uint32_t* flags, uint32_t n_chunks) {
   using C = CompactCfg<RB>;
   constexpr int LPP = C::LPP, RPS = C::RPS, U = C::U;
-  const int64_t w = blockIdx.x;
-  const int64_t slice = w / (2 * C::NCB);
-  const int t = (int)((w / C::NCB) % 2);
-  const int cb = (int)(w % C::NCB);
-  char* base = (t == 0 ? K : V) + slice * S * RB + cb * C::CB;
-  const bool meta = (t == 0 && cb == 0);
-  int32_t* fr = frame_idx + slice * S;
-  int32_t* pa = patch_idx + slice * S;
-  const int32_t* keep = keep_idx + slice * budget;
-  const int tid = threadIdx.x, sub = tid / LPP, lane = tid % LPP;
+  __shared__ uint32_t sh_ok;
+  const int tid = threadIdx.x;
+  {
+    const uint32_t walks = gridDim.x / n_chunks;
+    const uint32_t k = blockIdx.x / walks, w = blockIdx.x % walks;
+    const int64_t slice = w / C::PARTS;
+    const int part = (int)(w % C::PARTS);
+    const int64_t c0 = (int64_t)k * kChunkRows;
+    const int64_t c1 = min((int64_t)budget, c0 + kChunkRows);
+    const int32_t* keep = keep_idx + slice * budget;
+    const bool data = part < 2 * C::NCB;
 
-#pragma unroll 1
-  for (int64_t j0 = 0; j0 < budget; j0 += C::CH) {
+    // 1. loads
     Raw16 buf[U];
-    int32_t src[U], mf[U], mp[U];
+    int32_t src[U];
+    int32_t mval = 0, msrc = -1;
     bool bad = false;
+    char* base = nullptr;
+    int32_t* marr = nullptr;
+    const int sub = tid / LPP, lane = tid % LPP;
+    if (data) {
+      base = (part < C::NCB ? K : V) + slice * S * RB + (part % C::NCB) * C::CB;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t j = j0 + u * RPS + sub;
-      src[u] = -1;
-      if (j < budget) {
+      for (int u = 0; u < U; ++u) {
+        const int64_t j = c0 + u * RPS + sub;
+        src[u] = -1;
+        if (j < c1) {
+          const int32_t s = keep[j];
+          if (s < j || s >= n) {
+            bad = true;
+          } else if (s != j) {
+            src[u] = s;
+            buf[u] = load16(base + (int64_t)s * RB + lane * 16);
+          }
+        }
+      }
+    } else {
+      marr = (tid < kChunkRows ? frame_idx : patch_idx) + slice * S;
+      const int64_t j = c0 + (tid % kChunkRows);
+      if (j < c1) {
         const int32_t s = keep[j];
         if (s < j || s >= n) {
           bad = true;
         } else if (s != j) {
-          src[u] = s;
-          buf[u] = load16(base + (int64_t)s * RB + lane * 16);
-          if (meta && lane == 0) {
-            mf[u] = fr[s];
-            mp[u] = pa[s];
-          }
+          msrc = s;
+          mval = marr[s];
         }
       }
     }
-    if (bad && lane == 0) raise_error(err, 8u);
+    if (bad) raise_error(err, 8u);
     // Use every loaded register in an opaque statement: the compiler must wait
-    // for each load's data here, before the barrier, and cannot sink a load
-    // past it. After the barrier every wave's loads of this chunk have landed.
+    // for each load's data here, before the barrier. After the barrier every
+    // wave's loads of this chunk have landed.
 #pragma unroll
-    for (int u = 0; u < U; ++u) asm volatile("" ::"v"(buf[u].w[0]), "v"(mf[u]), "v"(mp[u]));
+    for (int u = 0; u < U; ++u) asm volatile("" ::"v"(buf[u].w[0]));
+    asm volatile("" ::"v"(mval));
     __syncthreads();
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t j = j0 + u * RPS + sub;
-      if (src[u] >= 0) {
-        store16(base + j * RB + lane * 16, buf[u]);
-        if (meta && lane == 0) {
-          fr[j] = mf[u];
-          pa[j] = mp[u];
+
+    // 2. publish
+    uint32_t* wflags = flags + (int64_t)w * n_chunks;
+    if (tid == 0) store_flag(&wflags[k], 1u);
+
+    // 3. wait for the earlier chunks of this walk that read rows in [c0, c1)
+    if (tid < kWave) {
+      bool ok = true;
+      for (uint32_t j0 = 0; j0 < k && ok; j0 += kWave) {
+        const uint32_t jc = j0 + tid;
+        bool need = false;
+        if (jc < k) {
+          const int32_t lo = keep[(int64_t)jc * kChunkRows];
+          const int32_t hi = keep[min((int64_t)budget, (int64_t)(jc + 1) * kChunkRows) - 1];
+          need = hi >= c0 && lo < c1;
+        }
+        for (uint32_t spins = 0;; ++spins) {
+          const bool pending = need && load_flag(&wflags[jc]) == 0u;
+          if (__ballot(pending) == 0) break;
+          if (spins >= kSpinLimit) {
+            ok = false;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
         }
       }
+      if (tid == 0) sh_ok = ok;
+    }
+    __syncthreads();
+
+    // 4. store
+    if (sh_ok) {
+      if (data) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (src[u] >= 0) store16(base + (c0 + u * RPS + sub) * RB + lane * 16, buf[u]);
+      } else if (msrc >= 0) {
+        marr[c0 + (tid % kChunkRows)] = mval;
+      }
+    } else if (tid == 0) {
+      raise_error(err, 32u);
     }
   }
 }

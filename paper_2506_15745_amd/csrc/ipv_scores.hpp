@@ -19,11 +19,14 @@ namespace ipv {
 // frame order (deterministic), then scales by 1/r_q. Positions with no recent
 // key get m_q = 0, which makes their TaR score 0.
 // LDS: slot[g * r + (frame - first_recent_frame)] = row of that key, or -1.
+// The first block of each slice also publishes the slice's first recent row
+// (n when the window is empty), which the sweep uses to skip recent keys.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
                                                       const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
                                                       int32_t r, int32_t p, int32_t blocks_per_slice,
-                                                      float* __restrict__ table, uint32_t* err) {
+                                                      float* __restrict__ table, int32_t* __restrict__ first_recent,
+                                                      uint32_t* err) {
   constexpr int EPL = Lane<T>::EPL;
   constexpr int LPR = D / EPL;
   constexpr int GROUPS = 256 / LPR;
@@ -43,6 +46,9 @@ __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, c
   for (int64_t t = t0 + tid; t < n; t += 256) {
     const int32_t f = frame_idx[base + t];
     if (f < thr) continue;
+    // the window's first row: the one recent row whose predecessor is not recent
+    // (or the scan start); with non-decreasing frame ids there is exactly one
+    if (q0 == 0 && (t == t0 || frame_idx[base + t - 1] < thr)) first_recent[slice] = (int32_t)t;
     const int32_t q = patch_idx[base + t];
     if (q < 0 || q >= p) {
       raise_error(err, 1u);
@@ -65,19 +71,29 @@ __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, c
   for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
   int cnt = 0;
   if (q < q1) {
-    for (int j = 0; j < r; ++j) {
-      const int32_t y = slot[g * r + j];
-      if (y < 0) continue;
-      ++cnt;
-      float f[EPL];
-      Lane<T>::decode(load16(K + (base + y) * D + lane * EPL), f);
-      float ss = 0.f;
+    // batches of 4 independent key loads, summed in frame order
+    for (int j0 = 0; j0 < r; j0 += 4) {
+      Raw16 raw[4];
+      int32_t y[4];
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
-      ss = group_sum<LPR>(ss);
-      const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+      for (int b = 0; b < 4; ++b) {
+        y[b] = j0 + b < r ? slot[g * r + j0 + b] : -1;
+        if (y[b] >= 0) raw[b] = load16(K + (base + y[b]) * D + lane * EPL);
+      }
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) acc[i] += f[i] * inv;
+      for (int b = 0; b < 4; ++b) {
+        if (y[b] < 0) continue;  // uniform within the lane group
+        ++cnt;
+        float f[EPL];
+        Lane<T>::decode(raw[b], f);
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
+        ss = group_sum<LPR>(ss);
+        const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) acc[i] += f[i] * inv;
+      }
     }
     const float scale = cnt ? 1.f / (float)cnt : 0.f;
     float* out = table + ((int64_t)slice * p + q) * D + lane * EPL;
@@ -89,59 +105,76 @@ __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, c
 }
 
 // ---------------------------------------------------------------- fused TaR + VaN sweep
-// Each row is read by a group of LPR lanes, 16 bytes per lane; a workgroup of
-// 256 threads covers GROUPS consecutive rows per step and U steps per tile,
-// issuing all of its K/V loads before any arithmetic. Workgroups are
-// renumbered so the tiles of one slice share an XCD (and the slice's m table
-// stays in that XCD's L2).
+// Rows are tiled over the (frame, patch) plane of the row space: row x is
+// taken as frame x / p, patch x % p. This covers every row exactly once for
+// any layout, and it is the true position of every row in a cache filled with
+// whole frames. A tile is GROUPS consecutive patch columns by U frames; each
+// lane group (LPR lanes, 16 bytes per lane) owns one column, so for every
+// frame step the workgroup reads GROUPS consecutive rows (contiguous bytes).
+//
+// A column's U rows normally share one patch, hence one m vector: the group
+// fetches m for the column's own patch position at the same time as the K/V
+// loads (no dependence on patch_idx), then checks every row's real patch_idx
+// and fetches the right m vector for any row where the two differ. The result
+// never depends on the layout; only the number of m fetches does.
+//
+// Rows at or after first_recent (the start of the recent window, published
+// per slice by the table kernel) are recent: TaR 0 and no K read.
 template <typename T, int D>
 struct SweepCfg {
   static constexpr int EPL = Lane<T>::EPL;
   static constexpr int LPR = D / EPL;
   static constexpr int GROUPS = 256 / LPR;
   static constexpr int U = 4;
-  static constexpr int TILE = GROUPS * U;
 };
 
+// grid: padded to a multiple of 8; work w = (slice * frame_blocks + frame block) * col_blocks + column block
 template <typename T, int D, bool TAR, bool VAN>
 __global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, const T* __restrict__ V,
-                                                     const int32_t* __restrict__ frame_idx,
                                                      const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
-                                                     int32_t r, int32_t p, const float* __restrict__ table,
+                                                     int32_t p, const float* __restrict__ table,
+                                                     const int32_t* __restrict__ first_recent,
                                                      float* __restrict__ tar, float* __restrict__ van,
-                                                     uint32_t* err, int32_t tiles_per_slice, uint32_t n_work) {
+                                                     uint32_t* err, int32_t col_blocks, int32_t frame_blocks,
+                                                     uint32_t n_work) {
   using C = SweepCfg<T, D>;
   constexpr int EPL = C::EPL, LPR = C::LPR, GROUPS = C::GROUPS, U = C::U;
   const uint32_t logical = xcd_logical_id(blockIdx.x, gridDim.x);
   if (logical >= n_work) return;
-  const int64_t slice = logical / tiles_per_slice;
-  const int64_t row0 = (int64_t)(logical % tiles_per_slice) * C::TILE;
+  const uint32_t tile = logical / col_blocks;
+  const int64_t slice = tile / frame_blocks;
+  const int32_t f0 = (int32_t)(tile % frame_blocks) * U;
+  const int32_t col = (int32_t)(logical % col_blocks) * GROUPS + threadIdx.x / LPR;
+  const int lane = threadIdx.x % LPR;
+  if (col >= p) return;  // the whole lane group idles: it is in no cross-lane sum
   const int64_t base = slice * S;
-  const int tid = threadIdx.x, g = tid / LPR, lane = tid % LPR;
-
-  int64_t thr = 0;
-  if (TAR) thr = (int64_t)frame_idx[base + n - 1] - r + 1;
+  const int32_t rec = TAR ? first_recent[slice] : n;
+  const float* mtab = table + (int64_t)slice * p * D + lane * EPL;
 
   Raw16 kr[U], vr[U];
-  int32_t fq[U], pq[U];
+  int32_t pq[U];
+  float4 ms[EPL / 4];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const int64_t x = row0 + u * GROUPS + g;
-    fq[u] = 0;
+    const int64_t x = (int64_t)(f0 + u) * p + col;
     pq[u] = -1;
     if (x < n) {
-      if (TAR) {
-        fq[u] = frame_idx[base + x];
+      if (TAR && x < rec) {
         pq[u] = patch_idx[base + x];
         kr[u] = load16(K + (base + x) * D + lane * EPL);
       }
       if (VAN) vr[u] = load16(V + (base + x) * D + lane * EPL);
     }
   }
+  const bool any_past = TAR && (int64_t)f0 * p + col < min(n, rec);
+  if (any_past) {
+#pragma unroll
+    for (int i = 0; i < EPL / 4; ++i) ms[i] = *reinterpret_cast<const float4*>(mtab + (int64_t)col * D + 4 * i);
+  }
   if (VAN) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t x = row0 + u * GROUPS + g;
+      const int64_t x = (int64_t)(f0 + u) * p + col;
       float f[EPL];
       float ss = 0.f;
       if (x < n) {
@@ -156,18 +189,25 @@ __global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, co
   if (TAR) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t x = row0 + u * GROUPS + g;
-      const bool past = x < n && (int64_t)fq[u] < thr;
-      const bool ok = past && pq[u] >= 0 && pq[u] < p;
+      const int64_t x = (int64_t)(f0 + u) * p + col;
+      const bool past = x < n && x < rec;
+      const int32_t q = pq[u];
+      const bool ok = past && q >= 0 && q < p;
       if (past && !ok && lane == 0) raise_error(err, 1u);
+      float4 m[EPL / 4];
+#pragma unroll
+      for (int i = 0; i < EPL / 4; ++i) m[i] = ms[i];
+      if (ok && q != col) {  // the row is not at its frame-plane position: exact lookup
+#pragma unroll
+        for (int i = 0; i < EPL / 4; ++i) m[i] = *reinterpret_cast<const float4*>(mtab + (int64_t)q * D + 4 * i);
+      }
       float dot = 0.f, kk = 0.f;
       if (ok) {
         float f[EPL];
         Lane<T>::decode(kr[u], f);
-        const float* m = table + ((int64_t)slice * p + pq[u]) * D + lane * EPL;
 #pragma unroll
         for (int i = 0; i < EPL; i += 4) {
-          const float4 mv = *reinterpret_cast<const float4*>(m + i);
+          const float4 mv = m[i / 4];
           dot += f[i] * mv.x + f[i + 1] * mv.y + f[i + 2] * mv.z + f[i + 3] * mv.w;
           kk += f[i] * f[i] + f[i + 1] * f[i + 1] + f[i + 2] * f[i + 2] + f[i + 3] * f[i + 3];
         }

@@ -26,7 +26,7 @@ LIB_PATH = os.path.join(HERE, "libipv.so")
 
 OK, ERR_NULL, ERR_ALIGN, ERR_SHAPE, ERR_DTYPE, ERR_BUDGET, ERR_ARG, ERR_WORKSPACE, ERR_HIP = range(9)
 BF16, F32 = 0, 1
-DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN = 1, 2, 4, 8, 16
+DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN, DEV_WAIT_TIMEOUT = 1, 2, 4, 8, 16, 32
 
 EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
            "ipv_compress", "ipv_compress_timed", "ipv_clear_device_errors", "ipv_read_device_errors",

@@ -187,3 +187,29 @@ def test_compaction_adversarial_patterns(dtype, D):
         assert np.array_equal(Vh[..., :C, :].view(np.uint8), V[..., keep1, :].view(np.uint8)), name
         assert np.array_equal(fh[..., :C], fr[..., keep1]) and np.array_equal(ph[..., :C], pa[..., keep1]), name
         assert np.array_equal(Kh[..., n:, :].view(np.uint8), K[..., n:, :].view(np.uint8)), name
+
+
+def test_workspace_reused_across_calls_of_different_sizes():
+    # the compaction's tickets, done counter and epoch reset themselves at the end
+    # of every call: one zero-filled workspace serves many calls, of any budget
+    from paper_2506_15745_amd import ipv
+    w = W.Workload(name="reuse", streams=1, layers=3, kv_heads=2, head_dim=128, grid_h=8, grid_w=8,
+                   n_tokens=64 * 40, budget=0, recent_frames=3, alphas=(0.5,), dtype=synth.BF16, seeds=(9,),
+                   rho_specs=(synth.RhoSpec(),))
+    K, V, fr, pa = cache_of(w)
+    shape = ipv.Shape(1, w.layers, w.kv_heads, w.head_dim, w.n_tokens, w.grid_h, w.grid_w, 0)
+    ws = ipv.alloc_workspace(shape, "cuda:0")
+    for i, budget in enumerate((1280, 200, 2559, 900, 1280, 640, 2000, 192)):
+        print("call", i, "budget", budget, flush=True)
+        Kd, Vd = P.to_device(K, "bf16"), P.to_device(V, "bf16")
+        fd, pd = P.to_device(fr), P.to_device(pa)
+        comp = ipv.Compressor(Kd, w.grid_h, w.grid_w, budget)
+        comp.ws = ws
+        comp.compress(Kd, Vd, fd, pd, w.n_tokens, 0.5, w.recent_frames)
+        torch.cuda.synchronize()
+        assert ipv.ipv_read_device_errors(ws) == 0
+        keep = comp.keep_idx.cpu().numpy()
+        got = P.GpuPass(comp.tar.cpu().numpy(), comp.van.cpu().numpy(), keep, P.to_host(Kd), P.to_host(Vd),
+                        P.to_host(fd), P.to_host(pd), 0)
+        P.check_ascending(keep, w.n_tokens)
+        P.oracle_gather_equal(K, V, fr, pa, w.n_tokens, keep, got)
