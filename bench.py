@@ -29,6 +29,8 @@ import synth  # noqa: E402
 from synth import workloads as W  # noqa: E402
 
 METRIC = "compression-pass latency (us) + achieved HBM GB/s (% of peak), 1 MI355X"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = os.path.join(ROOT, "paper_2506_15745_amd", "csrc")
 PEAK_HBM_GBPS = 8000.0
 STEP_NAMES = ("recent_table", "score_sweep", "pool", "select", "compact")
 
@@ -83,6 +85,103 @@ def cpu_baseline(w, K, V, fr, pa, alpha, seconds):
             "sample": "whole %s pass, median of %d runs" % (w.name, len(times))}
 
 
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources: counter readings are valid only for this code."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_SOURCES)):
+        with open(os.path.join(KERNEL_SOURCES, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(step: str):
+    """HBM bytes per launch of a step's kernel, from the committed counter
+    readings (rocprofv3 FETCH_SIZE/WRITE_SIZE, scaled by the copy-kernel
+    calibration), or None when they were taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    e = t.get("kernels", {}).get(step)
+    return None if e is None else int(e["fetch_bytes"] + e["write_bytes"])
+
+
+def summarize(paths):
+    """Text summary of rocprofv3 result databases (kernel trace or counters)."""
+    import sqlite3
+    for path in paths:
+        con = sqlite3.connect(path)
+        print("# %s" % os.path.basename(path))
+        try:
+            rows = con.execute("select counter_name, kernel_name, count(*), avg(value) from counters_collection "
+                               "group by counter_name, kernel_name order by counter_name, kernel_name").fetchall()
+        except sqlite3.Error:
+            rows = []
+        if rows:
+            print("%-12s %8s %14s  %s" % ("counter", "calls", "avg per call", "kernel"))
+            for c, k, n, v in rows:
+                print("%-12s %8d %14.1f  %s" % (c, n, v, k[:110]))
+            continue
+        rows = con.execute("select name, count(*), avg(duration), min(duration), max(duration), sum(duration) "
+                           "from kernels group by name order by sum(duration) desc").fetchall()
+        total = sum(r[5] for r in rows) or 1
+        print("%8s %10s %10s %10s %7s  %s" % ("calls", "avg_us", "min_us", "max_us", "time%", "kernel"))
+        for name, n, avg, mn, mx, tot in rows:
+            print("%8d %10.2f %10.2f %10.2f %6.1f%%  %s" % (n, avg / 1e3, mn / 1e3, mx / 1e3, 100 * tot / total,
+                                                          name[:110]))
+
+
+STEP_KERNELS = {"recent_table": "k_recent_table<", "score_sweep": "k_score_sweep<", "select": "k_select<",
+                "compact": "k_compact<"}
+
+
+def write_traffic(fetch_db, write_db, cal_fetch_db, cal_write_db):
+    """profiles/traffic.json from two counter runs of the benchmark and two of
+    the copy probe: per step kernel, HBM bytes per launch = FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) times the factor that maps the copy
+    probe's counters onto its known size."""
+    import sqlite3
+
+    def per_kernel(path, counter):
+        con = sqlite3.connect(path)
+        rows = con.execute("select kernel_name, avg(value) from counters_collection where counter_name = ? "
+                           "group by kernel_name", (counter,)).fetchall()
+        return {k: v for k, v in rows}
+
+    copy_kib = (360 << 20) / 1024
+    cal = {}
+    for counter, db in (("FETCH_SIZE", cal_fetch_db), ("WRITE_SIZE", cal_write_db)):
+        copies = [v for k, v in per_kernel(db, counter).items() if "copyBuffer" in k]
+        cal[counter] = copy_kib / max(copies)
+    fetch, write = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
+    out = {"source_hash": kernel_source_hash(), "calibration": cal, "kernels": {}}
+    for step, pat in STEP_KERNELS.items():
+        f = [v for k, v in fetch.items() if pat in k]
+        w_ = [v for k, v in write.items() if pat in k]
+        if f and w_:
+            out["kernels"][step] = {"fetch_bytes": int(f[0] * cal["FETCH_SIZE"] * 1024),
+                                    "write_bytes": int(w_[0] * cal["WRITE_SIZE"] * 1024)}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out))
+
+
+def copy_probe():
+    """A plain device-to-device copy of 360 MiB, three times: the known-size
+    reference for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.ones((360 << 20) // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": src.numel() * 4, "copies": 3}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -92,12 +191,26 @@ def main():
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
+    ap.add_argument("--summarize", nargs="+", metavar="DB", help="print summaries of rocprofv3 result databases")
+    ap.add_argument("--traffic", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "CAL_FETCH_DB", "CAL_WRITE_DB"),
+                    help="write profiles/traffic.json from counter runs")
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args.summarize)
+        return
+    if args.traffic:
+        write_traffic(*args.traffic)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the pass shards by (stream, layer, KV head) with no communication, "
               "so only --gpus 1 is supported", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe()
+        return
 
     import torch
     from paper_2506_15745_amd import ipv
@@ -206,7 +319,8 @@ def main():
         "step_us_mean": {k: round(v, 2) for k, v in step_us.items()},
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None},
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "algorithmic_bytes": algo_by_step[dom], "traffic": measured_traffic(dom)},
         "device_errors": errors,
     }
     if not args.no_cpu_baseline:

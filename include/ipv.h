@@ -87,7 +87,7 @@ enum {
   IPV_DEV_RECENT_OVER = 4u,    /* recent window larger than the budget: keep_idx set to 0..C-1 */
   IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n): row j was not moved */
   IPV_DEV_NAN = 16u,           /* a candidate score is NaN: its rank is unspecified */
-  IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired (a workspace shared by
+  IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired (e.g. a workspace shared by
                                   overlapping calls); its rows were not moved */
 };
 

@@ -24,6 +24,8 @@ namespace {
 constexpr int32_t kMaxRows = 65536;  // select: 1024 threads x 64 row flags
 constexpr int64_t kMaxWindowRows = 65536;        // r * p: recent rows scanned per table block
 constexpr int32_t kMaxRecentFrames = 256;
+constexpr int kCompactThreads = 256;
+constexpr int kMinChunkRows = kCompactThreads / 2;  // smallest compaction chunk of any kernel
 
 struct Dims {
   int64_t B, L, H, S, D, p, slices;
@@ -81,7 +83,7 @@ ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
 // flags  walks * chunks    uint32 per compaction chunk (1 once its rows are loaded)
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 int64_t compact_parts(const Dims& d) { return 2 * std::max<int64_t>(1, d.D * d.elem / 128) + 1; }
-int64_t max_chunks(const Dims& d) { return (d.S + kChunkRows - 1) / kChunkRows; }
+int64_t max_chunks(const Dims& d) { return (d.S + kMinChunkRows - 1) / kMinChunkRows; }
 size_t table_offset() { return kWsHeader; }
 size_t table_bytes(const Dims& d) { return (size_t)(d.slices * d.p * d.D) * sizeof(float); }
 size_t first_offset(const Dims& d) { return up256(table_offset() + table_bytes(d)); }
@@ -204,12 +206,13 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
 template <int RB>
 ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
                        int32_t budget, void* ws, hipStream_t st) {
-  const uint32_t chunks = (uint32_t)((budget + kChunkRows - 1) / kChunkRows);
-  const int64_t total = d.slices * CompactCfg<RB>::PARTS * chunks;
+  using C = CompactCfg<RB, kCompactThreads>;
+  const uint32_t chunks = (uint32_t)((budget + C::CH - 1) / C::CH);
+  const int64_t total = d.slices * C::PARTS * chunks;
   k_clear_flags<<<dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), total);
-  k_compact<RB><<<dim3((uint32_t)total), dim3(256), 0, st>>>(static_cast<char*>(K), static_cast<char*>(V), fr, pa,
-                                                             d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
-                                                             chunks);
+  k_compact<RB, kCompactThreads><<<dim3((uint32_t)total), dim3(kCompactThreads), 0, st>>>(
+      static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
+      chunks);
   return launched();
 }
 

@@ -3,7 +3,8 @@
 //
 // The rows of a slice form independent "walks": each 128-byte column block of
 // K, each of V, and the metadata pair. A walk's output rows are cut into
-// chunks of CH rows and every chunk is one workgroup, so the whole copy runs
+// chunks of CH rows and every chunk is one workgroup (CH = half the
+// workgroup size), so the whole copy runs
 // in parallel. The in-place hazard: a chunk writes rows [c0, c1) that an
 // earlier chunk of the same walk may still have to read (keep[j] >= j, so a
 // chunk's sources lie at or after its own rows, never before). Hence:
@@ -28,17 +29,18 @@
 
 namespace ipv {
 
-constexpr int kChunkRows = 128;
 constexpr uint32_t kSpinLimit = 1u << 20;
 
-template <int RB>  // bytes per row
+template <int RB, int NT>  // bytes per row, threads per chunk
 struct CompactCfg {
+  static constexpr int CH = NT / 2;               // rows per chunk (the metadata walk: 2 arrays x CH rows)
   static constexpr int CB = RB < 128 ? RB : 128;  // bytes per column block (one cache line)
   static constexpr int NCB = RB / CB;             // column blocks per row
   static constexpr int LPP = CB / 16;             // lanes per row piece
-  static constexpr int RPS = 256 / LPP;           // rows per step
-  static constexpr int U = kChunkRows / RPS;      // steps per chunk
+  static constexpr int RPS = NT / LPP;            // rows per step
+  static constexpr int U = CH / RPS;              // steps per chunk
   static constexpr int PARTS = 2 * NCB + 1;       // walks per slice: K blocks, V blocks, metadata
+  static_assert(U >= 1 && U * RPS == CH, "chunk shape");
 };
 
 __device__ inline uint32_t load_flag(const uint32_t* p) {
@@ -49,121 +51,128 @@ __device__ inline void store_flag(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Zero `count` chunk flags.
+// Zero `count` words.
 __global__ void k_clear_flags(uint32_t* flags, int64_t count) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) flags[i] = 0u;
 }
 
-// grid: slices * PARTS * n_chunks workgroups of 256 threads, id = chunk * walks + walk
-template <int RB>
-__global__ __launch_bounds__(256) void k_compact(char* __restrict__ K, char* __restrict__ V,
-                                                 int32_t* __restrict__ frame_idx, int32_t* __restrict__ patch_idx,
-                                                 int64_t S, int32_t n, int32_t budget,
-                                                 const int32_t* __restrict__ keep_idx, uint32_t* err,
-                                                 uint32_t* flags, uint32_t n_chunks) {
-  using C = CompactCfg<RB>;
-  constexpr int LPP = C::LPP, RPS = C::RPS, U = C::U;
-  __shared__ uint32_t sh_ok;
+// Chunk k of walk `part` of `slice` with NT threads. wflags: the walk's flags
+// (one per chunk, zero at kernel start). ok_sh: one word of LDS.
+template <int RB, int NT>
+__device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __restrict__ V, int32_t* __restrict__ frame_idx,
+                              int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t budget,
+                              const int32_t* __restrict__ keep_idx, uint32_t* err, uint32_t* wflags,
+                              int64_t slice, int part, uint32_t k, uint32_t* ok_sh) {
+  using C = CompactCfg<RB, NT>;
+  constexpr int LPP = C::LPP, RPS = C::RPS, U = C::U, CH = C::CH;
   const int tid = threadIdx.x;
-  {
-    const uint32_t walks = gridDim.x / n_chunks;
-    const uint32_t k = blockIdx.x / walks, w = blockIdx.x % walks;
-    const int64_t slice = w / C::PARTS;
-    const int part = (int)(w % C::PARTS);
-    const int64_t c0 = (int64_t)k * kChunkRows;
-    const int64_t c1 = min((int64_t)budget, c0 + kChunkRows);
-    const int32_t* keep = keep_idx + slice * budget;
-    const bool data = part < 2 * C::NCB;
+  const int64_t c0 = (int64_t)k * CH;
+  const int64_t c1 = min((int64_t)budget, c0 + CH);
+  const int32_t* keep = keep_idx + slice * budget;
+  const bool data = part < 2 * C::NCB;
 
-    // 1. loads
-    Raw16 buf[U];
-    int32_t src[U];
-    int32_t mval = 0, msrc = -1;
-    bool bad = false;
-    char* base = nullptr;
-    int32_t* marr = nullptr;
-    const int sub = tid / LPP, lane = tid % LPP;
-    if (data) {
-      base = (part < C::NCB ? K : V) + slice * S * RB + (part % C::NCB) * C::CB;
+  // 1. loads
+  Raw16 buf[U];
+  int32_t src[U];
+  int32_t mval = 0, msrc = -1;
+  bool bad = false;
+  char* base = nullptr;
+  int32_t* marr = nullptr;
+  const int sub = tid / LPP, lane = tid % LPP;
+  if (data) {
+    base = (part < C::NCB ? K : V) + slice * S * RB + (part % C::NCB) * C::CB;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t j = c0 + u * RPS + sub;
-        src[u] = -1;
-        if (j < c1) {
-          const int32_t s = keep[j];
-          if (s < j || s >= n) {
-            bad = true;
-          } else if (s != j) {
-            src[u] = s;
-            buf[u] = load16(base + (int64_t)s * RB + lane * 16);
-          }
-        }
-      }
-    } else {
-      marr = (tid < kChunkRows ? frame_idx : patch_idx) + slice * S;
-      const int64_t j = c0 + (tid % kChunkRows);
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = c0 + u * RPS + sub;
+      src[u] = -1;
       if (j < c1) {
         const int32_t s = keep[j];
         if (s < j || s >= n) {
           bad = true;
         } else if (s != j) {
-          msrc = s;
-          mval = marr[s];
+          src[u] = s;
+          buf[u] = load16(base + (int64_t)s * RB + lane * 16);
         }
       }
     }
-    if (bad) raise_error(err, 8u);
-    // Use every loaded register in an opaque statement: the compiler must wait
-    // for each load's data here, before the barrier. After the barrier every
-    // wave's loads of this chunk have landed.
-#pragma unroll
-    for (int u = 0; u < U; ++u) asm volatile("" ::"v"(buf[u].w[0]));
-    asm volatile("" ::"v"(mval));
-    __syncthreads();
-
-    // 2. publish
-    uint32_t* wflags = flags + (int64_t)w * n_chunks;
-    if (tid == 0) store_flag(&wflags[k], 1u);
-
-    // 3. wait for the earlier chunks of this walk that read rows in [c0, c1)
-    if (tid < kWave) {
-      bool ok = true;
-      for (uint32_t j0 = 0; j0 < k && ok; j0 += kWave) {
-        const uint32_t jc = j0 + tid;
-        bool need = false;
-        if (jc < k) {
-          const int32_t lo = keep[(int64_t)jc * kChunkRows];
-          const int32_t hi = keep[min((int64_t)budget, (int64_t)(jc + 1) * kChunkRows) - 1];
-          need = hi >= c0 && lo < c1;
-        }
-        for (uint32_t spins = 0;; ++spins) {
-          const bool pending = need && load_flag(&wflags[jc]) == 0u;
-          if (__ballot(pending) == 0) break;
-          if (spins >= kSpinLimit) {
-            ok = false;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
+  } else {
+    marr = (tid < CH ? frame_idx : patch_idx) + slice * S;
+    const int64_t j = c0 + (tid % CH);
+    if (j < c1) {
+      const int32_t s = keep[j];
+      if (s < j || s >= n) {
+        bad = true;
+      } else if (s != j) {
+        msrc = s;
+        mval = marr[s];
       }
-      if (tid == 0) sh_ok = ok;
-    }
-    __syncthreads();
-
-    // 4. store
-    if (sh_ok) {
-      if (data) {
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          if (src[u] >= 0) store16(base + (c0 + u * RPS + sub) * RB + lane * 16, buf[u]);
-      } else if (msrc >= 0) {
-        marr[c0 + (tid % kChunkRows)] = mval;
-      }
-    } else if (tid == 0) {
-      raise_error(err, 32u);
     }
   }
+  if (bad) raise_error(err, 8u);
+  // Use every loaded register in an opaque statement: the compiler must wait
+  // for each load's data here, before the barrier. After the barrier every
+  // wave's loads of this chunk have landed.
+#pragma unroll
+  for (int u = 0; u < U; ++u) asm volatile("" ::"v"(buf[u].w[0]));
+  asm volatile("" ::"v"(mval));
+  __syncthreads();
+
+  // 2. publish
+  if (tid == 0) store_flag(&wflags[k], 1u);
+
+  // 3. wait for the earlier chunks of this walk that read rows in [c0, c1)
+  if (tid < kWave) {
+    bool ok = true;
+    for (uint32_t j0 = 0; j0 < k && ok; j0 += kWave) {
+      const uint32_t jc = j0 + tid;
+      bool need = false;
+      if (jc < k) {
+        const int32_t lo = keep[(int64_t)jc * CH];
+        const int32_t hi = keep[min((int64_t)budget, (int64_t)(jc + 1) * CH) - 1];
+        need = hi >= c0 && lo < c1;
+      }
+      for (uint32_t spins = 0;; ++spins) {
+        const bool pending = need && load_flag(&wflags[jc]) == 0u;
+        if (__ballot(pending) == 0) break;
+        if (spins >= kSpinLimit) {
+          ok = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    if (tid == 0) *ok_sh = ok;
+  }
+  __syncthreads();
+
+  // 4. store
+  if (*ok_sh) {
+    if (data) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (src[u] >= 0) store16(base + (c0 + u * RPS + sub) * RB + lane * 16, buf[u]);
+    } else if (msrc >= 0) {
+      marr[c0 + (tid % CH)] = mval;
+    }
+  } else if (tid == 0) {
+    raise_error(err, 32u);
+  }
+}
+
+// grid: slices * PARTS * n_chunks workgroups of NT threads, id = chunk * walks + walk
+template <int RB, int NT>
+__global__ __launch_bounds__(NT) void k_compact(char* __restrict__ K, char* __restrict__ V,
+                                                int32_t* __restrict__ frame_idx, int32_t* __restrict__ patch_idx,
+                                                int64_t S, int32_t n, int32_t budget,
+                                                const int32_t* __restrict__ keep_idx, uint32_t* err,
+                                                uint32_t* flags, uint32_t n_chunks) {
+  using C = CompactCfg<RB, NT>;
+  __shared__ uint32_t ok_sh;
+  const uint32_t walks = gridDim.x / n_chunks;
+  const uint32_t k = blockIdx.x / walks, w = blockIdx.x % walks;
+  compact_chunk<RB, NT>(K, V, frame_idx, patch_idx, S, n, budget, keep_idx, err, flags + (int64_t)w * n_chunks,
+                        w / C::PARTS, (int)(w % C::PARTS), k, &ok_sh);
 }
 
 }  // namespace ipv

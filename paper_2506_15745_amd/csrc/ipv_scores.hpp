@@ -14,36 +14,31 @@
 namespace ipv {
 
 // ---------------------------------------------------------------- recent-key table
-// One workgroup per (slice, block of patch positions). Each lane group of
-// LPR lanes owns one patch position q and sums the unit recent keys at q in
-// frame order (deterministic), then scales by 1/r_q. Positions with no recent
-// key get m_q = 0, which makes their TaR score 0.
-// LDS: slot[g * r + (frame - first_recent_frame)] = row of that key, or -1.
-// The first block of each slice also publishes the slice's first recent row
-// (n when the window is empty), which the sweep uses to skip recent keys.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
-                                                      const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
-                                                      int32_t r, int32_t p, int32_t blocks_per_slice,
-                                                      float* __restrict__ table, int32_t* __restrict__ first_recent,
-                                                      uint32_t* err) {
+// One block of NT threads per (slice, GROUPS = NT / LPR patch positions).
+// Each lane group of LPR lanes owns one patch position q and sums the unit
+// recent keys at q in frame order (deterministic), then scales by 1/r_q.
+// Positions with no recent key get m_q = 0, which makes their TaR score 0.
+// slot (LDS, GROUPS * r ints): slot[g * r + (frame - first recent frame)] =
+// row of that key, or -1. The block with q0 == 0 also publishes the slice's
+// first recent row, which the sweep uses to skip recent keys.
+template <typename T, int D, int NT>
+__device__ __forceinline__ void table_block(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
+                            const int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t r, int32_t p,
+                            int64_t slice, int32_t q0, float* __restrict__ table, int32_t* __restrict__ first_recent,
+                            uint32_t* err, int32_t* slot) {
   constexpr int EPL = Lane<T>::EPL;
   constexpr int LPR = D / EPL;
-  constexpr int GROUPS = 256 / LPR;
-  extern __shared__ int32_t slot[];
-
+  constexpr int GROUPS = NT / LPR;
   const int tid = threadIdx.x;
-  const int64_t slice = blockIdx.x / blocks_per_slice;
-  const int32_t q0 = (blockIdx.x % blocks_per_slice) * GROUPS;
   const int32_t q1 = min(p, q0 + GROUPS);
   const int64_t base = slice * S;
   const int64_t thr = (int64_t)frame_idx[base + n - 1] - r + 1;
 
-  for (int i = tid; i < GROUPS * r; i += 256) slot[i] = -1;
+  for (int i = tid; i < GROUPS * r; i += NT) slot[i] = -1;
   __syncthreads();
   // A recent frame holds at most p rows, so the window lies in the last r*p rows.
   const int64_t t0 = max((int64_t)0, (int64_t)n - (int64_t)r * p);
-  for (int64_t t = t0 + tid; t < n; t += 256) {
+  for (int64_t t = t0 + tid; t < n; t += NT) {
     const int32_t f = frame_idx[base + t];
     if (f < thr) continue;
     // the window's first row: the one recent row whose predecessor is not recent
@@ -104,6 +99,18 @@ __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, c
   }
 }
 
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
+                                                      const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                      int32_t r, int32_t p, int32_t blocks_per_slice,
+                                                      float* __restrict__ table, int32_t* __restrict__ first_recent,
+                                                      uint32_t* err) {
+  constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
+  extern __shared__ int32_t slot[];
+  table_block<T, D, 256>(K, frame_idx, patch_idx, S, n, r, p, blockIdx.x / blocks_per_slice,
+                         (int32_t)(blockIdx.x % blocks_per_slice) * GROUPS, table, first_recent, err, slot);
+}
+
 // ---------------------------------------------------------------- fused TaR + VaN sweep
 // Rows are tiled over the (frame, patch) plane of the row space: row x is
 // taken as frame x / p, patch x % p. This covers every row exactly once for
@@ -128,27 +135,20 @@ struct SweepCfg {
   static constexpr int U = 4;
 };
 
-// grid: padded to a multiple of 8; work w = (slice * frame_blocks + frame block) * col_blocks + column block
+// One tile: 256 threads (tid in [0, 256)), columns [colblock * GROUPS, +GROUPS),
+// frames [f0, f0 + U). rec = the slice's first recent row.
 template <typename T, int D, bool TAR, bool VAN>
-__global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, const T* __restrict__ V,
-                                                     const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
-                                                     int32_t p, const float* __restrict__ table,
-                                                     const int32_t* __restrict__ first_recent,
-                                                     float* __restrict__ tar, float* __restrict__ van,
-                                                     uint32_t* err, int32_t col_blocks, int32_t frame_blocks,
-                                                     uint32_t n_work) {
+__device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __restrict__ V, const int32_t* __restrict__ patch_idx,
+                           int64_t S, int32_t n, int32_t p, const float* __restrict__ table, int32_t rec,
+                           float* __restrict__ tar, float* __restrict__ van, uint32_t* err, int64_t slice,
+                           int32_t f0, int32_t colblock, int tid) {
   using C = SweepCfg<T, D>;
   constexpr int EPL = C::EPL, LPR = C::LPR, GROUPS = C::GROUPS, U = C::U;
-  const uint32_t logical = xcd_logical_id(blockIdx.x, gridDim.x);
-  if (logical >= n_work) return;
-  const uint32_t tile = logical / col_blocks;
-  const int64_t slice = tile / frame_blocks;
-  const int32_t f0 = (int32_t)(tile % frame_blocks) * U;
-  const int32_t col = (int32_t)(logical % col_blocks) * GROUPS + threadIdx.x / LPR;
-  const int lane = threadIdx.x % LPR;
+  const int32_t col = colblock * GROUPS + tid / LPR;
+  const int lane = tid % LPR;
   if (col >= p) return;  // the whole lane group idles: it is in no cross-lane sum
   const int64_t base = slice * S;
-  const int32_t rec = TAR ? first_recent[slice] : n;
+  if (!TAR) rec = n;
   const float* mtab = table + (int64_t)slice * p * D + lane * EPL;
 
   Raw16 kr[U], vr[U];
@@ -221,6 +221,26 @@ __global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, co
       }
     }
   }
+}
+
+// grid: padded to a multiple of 8; work w = (slice * frame_blocks + frame block) * col_blocks + column block
+template <typename T, int D, bool TAR, bool VAN>
+__global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, const T* __restrict__ V,
+                                                     const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                     int32_t p, const float* __restrict__ table,
+                                                     const int32_t* __restrict__ first_recent,
+                                                     float* __restrict__ tar, float* __restrict__ van,
+                                                     uint32_t* err, int32_t col_blocks, int32_t frame_blocks,
+                                                     uint32_t n_work) {
+  using C = SweepCfg<T, D>;
+  const uint32_t logical = xcd_logical_id(blockIdx.x, gridDim.x);
+  if (logical >= n_work) return;
+  const uint32_t tile = logical / col_blocks;
+  const int64_t slice = tile / frame_blocks;
+  const int32_t f0 = (int32_t)(tile % frame_blocks) * C::U;
+  const int32_t rec = TAR ? first_recent[slice] : n;
+  sweep_tile<T, D, TAR, VAN>(K, V, patch_idx, S, n, p, table, rec, tar, van, err, slice, f0,
+                             (int32_t)(logical % col_blocks), threadIdx.x);
 }
 
 // ---------------------------------------------------------------- adaptive pooling

@@ -45,7 +45,7 @@ __device__ inline int32_t wave_inclusive_scan(int32_t v, int lane) {
 
 // Exclusive prefix sum over the workgroup in thread order; *total gets the sum.
 template <int NT>
-__device__ inline int32_t block_exclusive_scan(int32_t v, SelShared<NT>& sh, int32_t* total) {
+__device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, SelShared<NT>& sh, int32_t* total) {
   constexpr int NW = NT / kWave;
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int32_t incl = wave_inclusive_scan(v, lane);
@@ -67,7 +67,7 @@ __device__ inline int32_t block_exclusive_scan(int32_t v, SelShared<NT>& sh, int
 // Top-k of the candidate rows (bits of `cand`) by key; returns this thread's
 // picks. 0 < k <= number of candidates.
 template <int NT, int RPT>
-__device__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64_t cand, int32_t k, SelShared<NT>& sh) {
+__device__ __forceinline__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64_t cand, int32_t k, SelShared<NT>& sh) {
   constexpr int NW = NT / kWave;
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   // bits shared by every candidate key
@@ -157,7 +157,7 @@ __device__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64_t cand, int32_t
 }
 
 template <int RPT>
-__device__ inline void load_row_run(const void* __restrict__ src, int64_t row0, int32_t n, bool vec,
+__device__ __forceinline__ void load_row_run(const void* __restrict__ src, int64_t row0, int32_t n, bool vec,
                                     uint32_t (&out)[RPT]) {
   const uint32_t* s = static_cast<const uint32_t*>(src);
   if (vec && row0 + RPT <= n) {
@@ -175,15 +175,14 @@ __device__ inline void load_row_run(const void* __restrict__ src, int64_t row0, 
   }
 }
 
-// vec: every slice's row 0 is 16-byte aligned (capacity % 4 == 0), RPT % 4 == 0
+// One slice with NT threads. vec: every slice's row 0 is 16-byte aligned
+// (capacity % 4 == 0) so row runs load 16 bytes at a time.
 template <int NT, int RPT>
-__global__ __launch_bounds__(NT) void k_select(const float* __restrict__ tar, const float* __restrict__ van,
-                                               const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
-                                               int32_t budget, int32_t tar_total, int32_t r, int32_t vec,
-                                               int32_t* __restrict__ keep_idx, uint32_t* err) {
-  __shared__ SelShared<NT> sh;
+__device__ __forceinline__ void select_slice(const float* __restrict__ tar, const float* __restrict__ van,
+                             const int32_t* __restrict__ frame_idx, int64_t S, int32_t n, int32_t budget,
+                             int32_t tar_total, int32_t r, int32_t vec, int32_t* __restrict__ keep_idx,
+                             uint32_t* err, int64_t slice, SelShared<NT>& sh) {
   const int tid = threadIdx.x;
-  const int64_t slice = blockIdx.x;
   const int64_t base = slice * S;
   const int64_t row0 = (int64_t)tid * RPT;
   int32_t* keep = keep_idx + slice * budget;
@@ -227,40 +226,50 @@ __global__ __launch_bounds__(NT) void k_select(const float* __restrict__ tar, co
   __syncthreads();
   // with non-decreasing frame ids the window is the suffix starting at first_recent
   const int32_t n_recent = n - sh.first_recent;
-  if (sh.bad || n_recent > budget) {
+  const bool broken = sh.bad || n_recent > budget;
+  if (broken) {
     // metadata breaks the cache invariants: report, and keep rows 0..C-1 in place
     if (tid == 0) raise_error(err, sh.bad ? 2u : 4u);
     for (int32_t j = tid; j < budget; j += NT) keep[j] = j;
-    return;
-  }
-  const int32_t b_tar = max(0, tar_total - n_recent);
-  const int32_t b_van = budget - n_recent - b_tar;
-
-  const uint64_t past = valid & ~recent;
-  uint64_t pick_t = 0, pick_v = 0;
-  if (b_tar > 0) {
-    if (nan_t) raise_error(err, 16u);
-    pick_t = radix_top<NT, RPT>(kt, past, b_tar, sh);
-  }
-  if (b_van > 0) {
-    if (!kEarlyVan) {
-      load_row_run<RPT>(van + base, row0, n, vec, kv);
-#pragma unroll
-      for (int i = 0; i < RPT; ++i) {
-        nan_v |= ((past >> i) & 1ull) && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
-        kv[i] = order_key(__uint_as_float(kv[i]));
-      }
+  } else {
+    const int32_t b_tar = max(0, tar_total - n_recent);
+    const int32_t b_van = budget - n_recent - b_tar;
+    const uint64_t past = valid & ~recent;
+    uint64_t pick_t = 0, pick_v = 0;
+    if (b_tar > 0) {
+      if (nan_t) raise_error(err, 16u);
+      pick_t = radix_top<NT, RPT>(kt, past, b_tar, sh);
     }
-    if (nan_v) raise_error(err, 16u);
-    pick_v = radix_top<NT, RPT>(kv, past & ~pick_t, b_van, sh);
-  }
-  const uint64_t kept = recent | pick_t | pick_v;
-  int32_t total;
-  int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh, &total);
-  if (total != budget && tid == 0) raise_error(err, 16u);  // only reachable with NaN keys
+    if (b_van > 0) {
+      if (!kEarlyVan) {
+        load_row_run<RPT>(van + base, row0, n, vec, kv);
 #pragma unroll
-  for (int i = 0; i < RPT; ++i)
-    if (((kept >> i) & 1ull) && pos < budget) keep[pos++] = (int32_t)(row0 + i);
+        for (int i = 0; i < RPT; ++i) {
+          nan_v |= ((past >> i) & 1ull) && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
+          kv[i] = order_key(__uint_as_float(kv[i]));
+        }
+      }
+      if (nan_v) raise_error(err, 16u);
+      pick_v = radix_top<NT, RPT>(kv, past & ~pick_t, b_van, sh);
+    }
+    const uint64_t kept = recent | pick_t | pick_v;
+    int32_t total;
+    int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh, &total);
+    if (total != budget && tid == 0) raise_error(err, 16u);  // only reachable with NaN keys
+#pragma unroll
+    for (int i = 0; i < RPT; ++i)
+      if (((kept >> i) & 1ull) && pos < budget) keep[pos++] = (int32_t)(row0 + i);
+  }
+  __syncthreads();  // the caller may reuse sh
+}
+
+template <int NT, int RPT>
+__global__ __launch_bounds__(NT) void k_select(const float* __restrict__ tar, const float* __restrict__ van,
+                                               const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
+                                               int32_t budget, int32_t tar_total, int32_t r, int32_t vec,
+                                               int32_t* __restrict__ keep_idx, uint32_t* err) {
+  __shared__ SelShared<NT> sh;
+  select_slice<NT, RPT>(tar, van, frame_idx, S, n, budget, tar_total, r, vec, keep_idx, err, blockIdx.x, sh);
 }
 
 }  // namespace ipv
