@@ -187,9 +187,12 @@ template <int RPT>
 ipv_status run_select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
                       int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st) {
   // 16-byte row-run loads need every slice to start 16-byte aligned
-  const int32_t vec = (d.S % 4 == 0) ? 1 : 0;
-  k_select<kSelThreads, RPT><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget,
-                                                                                      tar_total, r, vec, keep, err);
+  if (d.S % 4 == 0)
+    k_select<kSelThreads, RPT, true><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(
+        tar, van, fr, d.S, n, budget, tar_total, r, keep, err);
+  else
+    k_select<kSelThreads, RPT, false><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(
+        tar, van, fr, d.S, n, budget, tar_total, r, keep, err);
   return launched();
 }
 

@@ -42,14 +42,86 @@ struct Lane<float> {
 
 __device__ inline Raw16 load16(const void* p) { return *reinterpret_cast<const Raw16*>(p); }
 
+// Buffer loads: a resource covers [base, base + bytes); a load past the end
+// returns zeros instead of faulting, so bounds need no branch (branches around
+// loads make the compiler wait for each load before the next is issued).
+constexpr int kBufferDword3 = 0x00020000;  // raw 32-bit data (gfx9 family)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferDword3);
+}
+
 __device__ inline void store16(void* p, const Raw16& v) { *reinterpret_cast<Raw16*>(p) = v; }
 
-// Sum over aligned groups of G lanes (G a power of two <= 64).
+// ---- cross-lane moves
+// DPP moves run in the vector ALU; __shfl_* goes through the LDS crossbar
+// (ds_bpermute) with far longer latency. DPP controls (GFX9 encoding):
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppRowShr = 0x110;     // + k: row_shr:k (within rows of 16 lanes)
+constexpr int kDppRowMirror = 0x140;  // lane l <- 15 - l within a row
+constexpr int kDppHalfMirror = 0x141; // lane l <- 7 - l within each 8 lanes
+
+template <int CTRL, bool BOUND_ZERO = false>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xf, 0xf, BOUND_ZERO);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(v)));
+}
+
+// Sum over aligned groups of G lanes (G a power of two <= 64); every lane of
+// a group gets the group's sum, the same in all of them. The first steps
+// pair lanes whose values are equal within smaller groups, so a mirror is an
+// exchange with the other half: xor 1, xor 2, (0..3 <-> 4..7), (0..7 <-> 8..15),
+// then xor 16 and xor 32 through the crossbar. A group is inactive as a whole
+// or active as a whole.
 template <int G>
-__device__ inline float group_sum(float v) {
-#pragma unroll
-  for (int m = G / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+__device__ __forceinline__ float group_sum(float v) {
+  if (G >= 2) v += dpp_f32<kDppXor1>(v);
+  if (G >= 4) v += dpp_f32<kDppXor2>(v);
+  if (G >= 8) v += dpp_f32<kDppHalfMirror>(v);
+  if (G >= 16) v += dpp_f32<kDppRowMirror>(v);
+  if (G >= 32) v += __shfl_xor(v, 16, kWave);
+  if (G >= 64) v += __shfl_xor(v, 32, kWave);
   return v;
+}
+
+// Inclusive prefix sum over the 64 lanes of a fully active wave: a
+// Hillis-Steele scan within each row of 16 lanes, then the totals of the
+// rows below are added.
+__device__ __forceinline__ int32_t wave_inclusive_scan(int32_t v) {
+  v += (int32_t)dpp_u32<kDppRowShr + 1, true>((uint32_t)v);
+  v += (int32_t)dpp_u32<kDppRowShr + 2, true>((uint32_t)v);
+  v += (int32_t)dpp_u32<kDppRowShr + 4, true>((uint32_t)v);
+  v += (int32_t)dpp_u32<kDppRowShr + 8, true>((uint32_t)v);
+  const int32_t r0 = __builtin_amdgcn_readlane(v, 15);
+  const int32_t r1 = __builtin_amdgcn_readlane(v, 31);
+  const int32_t r2 = __builtin_amdgcn_readlane(v, 47);
+  const int lane = (int)(threadIdx.x % kWave);
+  return v + (lane >= 16 ? r0 : 0) + (lane >= 32 ? r1 : 0) + (lane >= 48 ? r2 : 0);
+}
+
+// Minimum and maximum over the 64 lanes of a fully active wave (uniform result).
+__device__ __forceinline__ void wave_min_max(uint32_t& mn, uint32_t& mx) {
+  mn = min(mn, dpp_u32<kDppXor1>(mn));
+  mx = max(mx, dpp_u32<kDppXor1>(mx));
+  mn = min(mn, dpp_u32<kDppXor2>(mn));
+  mx = max(mx, dpp_u32<kDppXor2>(mx));
+  mn = min(mn, dpp_u32<kDppHalfMirror>(mn));
+  mx = max(mx, dpp_u32<kDppHalfMirror>(mx));
+  mn = min(mn, dpp_u32<kDppRowMirror>(mn));
+  mx = max(mx, dpp_u32<kDppRowMirror>(mx));
+  uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)mn, 0), b = (uint32_t)__builtin_amdgcn_readlane((int)mx, 0);
+#pragma unroll
+  for (int r = 16; r < kWave; r += 16) {
+    a = min(a, (uint32_t)__builtin_amdgcn_readlane((int)mn, r));
+    b = max(b, (uint32_t)__builtin_amdgcn_readlane((int)mx, r));
+  }
+  mn = a;
+  mx = b;
 }
 
 __device__ inline void raise_error(uint32_t* err, uint32_t bits) {

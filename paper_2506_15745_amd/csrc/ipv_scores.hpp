@@ -21,6 +21,18 @@ namespace ipv {
 // slot (LDS, GROUPS * r ints): slot[g * r + (frame - first recent frame)] =
 // row of that key, or -1. The block with q0 == 0 also publishes the slice's
 // first recent row, which the sweep uses to skip recent keys.
+//
+// Latency: every global load that does not depend on another is issued
+// before any result is used. A recent frame holds at most p rows, so the
+// window lies in the last r*p rows, t0 = n - r*p onwards; when those rows are
+// r whole frames in patch order (a cache that was filled frame by frame since
+// the last compaction), the key of recent frame j at position q is row
+// t0 + j*p + q. The first kSpecFrames of those rows are loaded before the
+// window is scanned, and used if the scan's slot table names the same rows;
+// otherwise (or for later frames) the keys are loaded from the slot rows.
+constexpr int kSpecFrames = 4;  // = the batch size of the summing loop below
+constexpr int kScanBatch = 4;
+
 template <typename T, int D, int NT>
 __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
                             const int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t r, int32_t p,
@@ -32,35 +44,67 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
   const int tid = threadIdx.x;
   const int32_t q1 = min(p, q0 + GROUPS);
   const int64_t base = slice * S;
-  const int64_t thr = (int64_t)frame_idx[base + n - 1] - r + 1;
+  const int g = tid / LPR, lane = tid % LPR;
+  const int32_t q = q0 + g;
+  const int64_t t0 = max((int64_t)0, (int64_t)n - (int64_t)r * p);
 
   for (int i = tid; i < GROUPS * r; i += NT) slot[i] = -1;
   __syncthreads();
-  // A recent frame holds at most p rows, so the window lies in the last r*p rows.
-  const int64_t t0 = max((int64_t)0, (int64_t)n - (int64_t)r * p);
-  for (int64_t t = t0 + tid; t < n; t += NT) {
-    const int32_t f = frame_idx[base + t];
-    if (f < thr) continue;
-    // the window's first row: the one recent row whose predecessor is not recent
-    // (or the scan start); with non-decreasing frame ids there is exactly one
-    if (q0 == 0 && (t == t0 || frame_idx[base + t - 1] < thr)) first_recent[slice] = (int32_t)t;
-    const int32_t q = patch_idx[base + t];
-    if (q < 0 || q >= p) {
-      raise_error(err, 1u);
-      continue;
+
+  // Loads take clamped (in-range) indices instead of branches, so that they
+  // are all in flight together; values of clamped loads are never used. The
+  // window scan reads NT * kScanBatch rows per batch (the whole window in the
+  // usual case); its loads are issued first, then the speculative key loads,
+  // and an empty asm statement takes the scan values, so the scan waits for
+  // its own loads only and the compiler cannot move them into the branches
+  // below. Errors are collected in a register and raised once.
+  int32_t f[kScanBatch], fprev[kScanBatch], pq[kScanBatch];
+  auto load_batch = [&](int64_t tb) {
+#pragma unroll
+    for (int b = 0; b < kScanBatch; ++b) {
+      const int64_t t = min(tb + (int64_t)b * NT + tid, (int64_t)n - 1);
+      f[b] = frame_idx[base + t];
+      pq[b] = patch_idx[base + t];
+      fprev[b] = frame_idx[base + max(t - 1, t0)];
     }
-    if (q < q0 || q >= q1) continue;
-    const int64_t fo = (int64_t)f - thr;
-    if (fo >= r) {  // a frame id above the last row's: ids decrease somewhere
-      raise_error(err, 2u);
-      continue;
+  };
+  const int64_t thr = (int64_t)frame_idx[base + n - 1] - r + 1;
+  uint32_t ebits = 0;
+  auto scan_batch = [&](int64_t tb) {
+#pragma unroll
+    for (int b = 0; b < kScanBatch; ++b) asm volatile("" ::"v"(f[b]), "v"(pq[b]), "v"(fprev[b]));
+#pragma unroll
+    for (int b = 0; b < kScanBatch; ++b) {
+      const int64_t t = tb + (int64_t)b * NT + tid;
+      if (t >= n || f[b] < thr) continue;
+      // the window's first row: the one recent row whose predecessor is not
+      // recent (or the scan start); with non-decreasing frame ids there is one
+      if (q0 == 0 && (t == t0 || fprev[b] < thr)) first_recent[slice] = (int32_t)t;
+      const int64_t fo = (int64_t)f[b] - thr;
+      if (pq[b] < 0 || pq[b] >= p) {
+        ebits |= 1u;
+      } else if (fo >= r) {  // a frame id above the last row's: ids decrease somewhere
+        ebits |= 2u;
+      } else if (pq[b] >= q0 && pq[b] < q1) {
+        if (atomicExch(&slot[(pq[b] - q0) * r + fo], (int32_t)t) != -1) ebits |= 2u;
+      }
     }
-    if (atomicExch(&slot[(q - q0) * r + fo], (int32_t)t) != -1) raise_error(err, 2u);
+  };
+  load_batch(t0);
+  Raw16 spec[kSpecFrames];
+#pragma unroll
+  for (int j = 0; j < kSpecFrames; ++j) {
+    const int64_t x = min(t0 + (int64_t)j * p + q, (int64_t)n - 1);
+    spec[j] = load16(K + (base + x) * D + lane * EPL);
   }
+  scan_batch(t0);
+  for (int64_t tb = t0 + (int64_t)NT * kScanBatch; tb < n; tb += (int64_t)NT * kScanBatch) {
+    load_batch(tb);
+    scan_batch(tb);
+  }
+  if (ebits) raise_error(err, ebits);
   __syncthreads();
 
-  const int g = tid / LPR, lane = tid % LPR;
-  const int32_t q = q0 + g;
   float acc[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
@@ -72,12 +116,17 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
       int32_t y[4];
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        y[b] = j0 + b < r ? slot[g * r + j0 + b] : -1;
-        if (y[b] >= 0) raw[b] = load16(K + (base + y[b]) * D + lane * EPL);
+        const int j = j0 + b;
+        y[b] = j < r ? slot[g * r + j] : -1;
+        if (y[b] < 0) continue;  // uniform within the lane group
+        if (j0 == 0 && y[b] == t0 + (int64_t)b * p + q)  // b < kSpecFrames: a fixed register
+          raw[b] = spec[b];
+        else
+          raw[b] = load16(K + (base + y[b]) * D + lane * EPL);
       }
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        if (y[b] < 0) continue;  // uniform within the lane group
+        if (y[b] < 0) continue;
         ++cnt;
         float f[EPL];
         Lane<T>::decode(raw[b], f);

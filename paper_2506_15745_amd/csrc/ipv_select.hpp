@@ -34,26 +34,17 @@ struct SelShared {
   int32_t bad;
 };
 
-__device__ inline int32_t wave_inclusive_scan(int32_t v, int lane) {
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int32_t t = __shfl_up(v, d, kWave);
-    if (lane >= d) v += t;
-  }
-  return v;
-}
-
 // Exclusive prefix sum over the workgroup in thread order; *total gets the sum.
 template <int NT>
 __device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, SelShared<NT>& sh, int32_t* total) {
   constexpr int NW = NT / kWave;
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
-  const int32_t incl = wave_inclusive_scan(v, lane);
+  const int32_t incl = wave_inclusive_scan(v);
   if (lane == kWave - 1) sh.wave_tot[w] = incl;
   __syncthreads();
   if (w == 0) {
     const int32_t t = lane < NW ? sh.wave_tot[lane] : 0;
-    const int32_t ti = wave_inclusive_scan(t, lane);
+    const int32_t ti = wave_inclusive_scan(t);
     if (lane < NW) sh.wave_off[lane] = ti - t;
     if (lane == NW - 1) sh.total = ti;
   }
@@ -78,11 +69,7 @@ __device__ __forceinline__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64
       mn = min(mn, key[i]);
       mx = max(mx, key[i]);
     }
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    mn = min(mn, (uint32_t)__shfl_xor((int)mn, d, kWave));
-    mx = max(mx, (uint32_t)__shfl_xor((int)mx, d, kWave));
-  }
+  wave_min_max(mn, mx);
   if (lane == 0) {
     sh.wave_min[w] = mn;
     sh.wave_max[w] = mx;
@@ -116,7 +103,7 @@ __device__ __forceinline__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64
 #pragma unroll
       for (int j = 0; j < 4; ++j) c[j] = (int32_t)sh.hist[cur][255 - 4 * lane - j];
       const int32_t s = c[0] + c[1] + c[2] + c[3];
-      const int32_t incl = wave_inclusive_scan(s, lane);
+      const int32_t incl = wave_inclusive_scan(s);
       const int32_t excl = incl - s;
       if (excl < remaining && remaining <= incl) {
         int32_t above = excl;
@@ -156,31 +143,34 @@ __device__ __forceinline__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64
   return pick;
 }
 
-template <int RPT>
-__device__ __forceinline__ void load_row_run(const void* __restrict__ src, int64_t row0, int32_t n, bool vec,
-                                    uint32_t (&out)[RPT]) {
-  const uint32_t* s = static_cast<const uint32_t*>(src);
-  if (vec && row0 + RPT <= n) {
+// Rows [row0, row0 + RPT) of one slice's column (S rows of 4 bytes); rows at
+// or past S read as 0. VEC: rows are 16-byte aligned (S % 4 == 0), so a run
+// lies wholly inside or wholly past the column and loads 16 bytes at a time.
+template <int RPT, bool VEC>
+__device__ __forceinline__ void load_row_run(const void* __restrict__ col, int64_t S, int64_t row0,
+                                             uint32_t (&out)[RPT]) {
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(col, (uint32_t)(S * 4));
+  if (VEC) {
 #pragma unroll
     for (int i = 0; i < RPT; i += 4) {
-      const Raw16 r = load16(s + row0 + i);
-      out[i] = r.w[0];
-      out[i + 1] = r.w[1];
-      out[i + 2] = r.w[2];
-      out[i + 3] = r.w[3];
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)((row0 + i) * 4), 0, 0);
+      out[i] = v[0];
+      out[i + 1] = v[1];
+      out[i + 2] = v[2];
+      out[i + 3] = v[3];
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) out[i] = row0 + i < n ? s[row0 + i] : 0u;
+    for (int i = 0; i < RPT; ++i) out[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)((row0 + i) * 4), 0, 0);
   }
 }
 
-// One slice with NT threads. vec: every slice's row 0 is 16-byte aligned
+// One slice with NT threads. VEC: every slice's row 0 is 16-byte aligned
 // (capacity % 4 == 0) so row runs load 16 bytes at a time.
-template <int NT, int RPT>
+template <int NT, int RPT, bool VEC>
 __device__ __forceinline__ void select_slice(const float* __restrict__ tar, const float* __restrict__ van,
                              const int32_t* __restrict__ frame_idx, int64_t S, int32_t n, int32_t budget,
-                             int32_t tar_total, int32_t r, int32_t vec, int32_t* __restrict__ keep_idx,
+                             int32_t tar_total, int32_t r, int32_t* __restrict__ keep_idx,
                              uint32_t* err, int64_t slice, SelShared<NT>& sh) {
   const int tid = threadIdx.x;
   const int64_t base = slice * S;
@@ -191,11 +181,14 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   // waits until the TaR stage is done, to stay within the register budget
   constexpr bool kEarlyVan = RPT <= 16;
   uint32_t fr[RPT], kt[RPT], kv[RPT];
-  load_row_run<RPT>(frame_idx + base, row0, n, vec, fr);
-  load_row_run<RPT>(tar + base, row0, n, vec, kt);
-  if (kEarlyVan) load_row_run<RPT>(van + base, row0, n, vec, kv);
-  const int32_t last = frame_idx[base + n - 1];
-  const int32_t before = (row0 > 0 && row0 <= n) ? frame_idx[base + row0 - 1] : INT32_MIN;
+  load_row_run<RPT, VEC>(frame_idx + base, S, row0, fr);
+  load_row_run<RPT, VEC>(tar + base, S, row0, kt);
+  if (kEarlyVan) load_row_run<RPT, VEC>(van + base, S, row0, kv);
+  const __amdgpu_buffer_rsrc_t frs = buffer_rsrc(frame_idx + base, (uint32_t)(S * 4));
+  const int32_t last = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)(n - 1) * 4u, 0, 0);
+  const int32_t prev_row = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)max(row0 - 1, (int64_t)0) * 4u,
+                                                                          0, 0);
+  const int32_t before = row0 > 0 ? prev_row : INT32_MIN;
   if (tid == 0) {
     sh.first_recent = n;
     sh.bad = 0;
@@ -242,7 +235,7 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
     }
     if (b_van > 0) {
       if (!kEarlyVan) {
-        load_row_run<RPT>(van + base, row0, n, vec, kv);
+        load_row_run<RPT, VEC>(van + base, S, row0, kv);
 #pragma unroll
         for (int i = 0; i < RPT; ++i) {
           nan_v |= ((past >> i) & 1ull) && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
@@ -263,13 +256,13 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   __syncthreads();  // the caller may reuse sh
 }
 
-template <int NT, int RPT>
+template <int NT, int RPT, bool VEC>
 __global__ __launch_bounds__(NT) void k_select(const float* __restrict__ tar, const float* __restrict__ van,
                                                const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
-                                               int32_t budget, int32_t tar_total, int32_t r, int32_t vec,
+                                               int32_t budget, int32_t tar_total, int32_t r,
                                                int32_t* __restrict__ keep_idx, uint32_t* err) {
   __shared__ SelShared<NT> sh;
-  select_slice<NT, RPT>(tar, van, frame_idx, S, n, budget, tar_total, r, vec, keep_idx, err, blockIdx.x, sh);
+  select_slice<NT, RPT, VEC>(tar, van, frame_idx, S, n, budget, tar_total, r, keep_idx, err, blockIdx.x, sh);
 }
 
 }  // namespace ipv
