@@ -120,9 +120,12 @@ uint32_t pad8(uint32_t x) { return (x + 7u) / 8u * 8u; }
 ipv_status no_mark() { return IPV_OK; }
 
 // between(): runs after the recent-key table is enqueued, before the sweep
+// zero_chunks > 0: the table kernel also zeroes the compaction flags for a
+// compaction of zero_chunks chunks per walk that follows in the same pass.
 template <typename T, int D, typename Between>
 ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
-                      int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between) {
+                      int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between,
+                      int64_t zero_chunks) {
   const bool do_tar = K != nullptr, do_van = V != nullptr;
   if (do_tar) {
     constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
@@ -130,7 +133,7 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
     const size_t lds = (size_t)GROUPS * r * sizeof(int32_t);
     k_recent_table<T, D><<<dim3((uint32_t)(d.slices * blocks)), dim3(256), lds, st>>>(
         static_cast<const T*>(K), fr, pa, d.S, n, r, (int32_t)d.p, blocks, ws_table(ws), ws_first(ws, d),
-        err_word(ws));
+        err_word(ws), zero_chunks > 0 ? ws_flags(ws, d) : nullptr, (int32_t)(compact_parts(d) * zero_chunks));
   }
   IPV_TRY(between());
   using C = SweepCfg<T, D>;
@@ -155,9 +158,10 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
 
 template <typename Between = ipv_status (*)()>
 ipv_status scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
-                  int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between = no_mark) {
+                  int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between = no_mark,
+                  int64_t zero_chunks = 0) {
 #define IPV_SCORES(T, DD) \
-  if (d.D == DD) return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between);
+  if (d.D == DD) return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between, zero_chunks);
   if (d.dtype == IPV_BF16) {
     IPV_SCORES(uint16_t, 32) IPV_SCORES(uint16_t, 64) IPV_SCORES(uint16_t, 128) IPV_SCORES(uint16_t, 256)
   } else {
@@ -206,13 +210,18 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
   return run_select<64>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
 }
 
+int64_t compact_chunks(int32_t budget) { return (budget + kMinChunkRows - 1) / kMinChunkRows; }
+
+// flags_zeroed: the pass's table kernel has zeroed the flags already
 template <int RB>
 ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
-                       int32_t budget, void* ws, hipStream_t st) {
+                       int32_t budget, void* ws, hipStream_t st, bool flags_zeroed) {
   using C = CompactCfg<RB, kCompactThreads>;
-  const uint32_t chunks = (uint32_t)((budget + C::CH - 1) / C::CH);
+  static_assert(C::CH == kMinChunkRows, "chunk rows");
+  const uint32_t chunks = (uint32_t)compact_chunks(budget);
   const int64_t total = d.slices * C::PARTS * chunks;
-  k_clear_flags<<<dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), total);
+  if (!flags_zeroed)
+    k_clear_flags<<<dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), total);
   k_compact<RB, kCompactThreads><<<dim3((uint32_t)total), dim3(kCompactThreads), 0, st>>>(
       static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
       chunks);
@@ -220,13 +229,13 @@ ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa
 }
 
 ipv_status compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
-                   int32_t budget, void* ws, hipStream_t st) {
+                   int32_t budget, void* ws, hipStream_t st, bool flags_zeroed = false) {
   switch (d.D * d.elem) {
-    case 64: return run_compact<64>(d, K, V, fr, pa, n, keep, budget, ws, st);
-    case 128: return run_compact<128>(d, K, V, fr, pa, n, keep, budget, ws, st);
-    case 256: return run_compact<256>(d, K, V, fr, pa, n, keep, budget, ws, st);
-    case 512: return run_compact<512>(d, K, V, fr, pa, n, keep, budget, ws, st);
-    case 1024: return run_compact<1024>(d, K, V, fr, pa, n, keep, budget, ws, st);
+    case 64: return run_compact<64>(d, K, V, fr, pa, n, keep, budget, ws, st, flags_zeroed);
+    case 128: return run_compact<128>(d, K, V, fr, pa, n, keep, budget, ws, st, flags_zeroed);
+    case 256: return run_compact<256>(d, K, V, fr, pa, n, keep, budget, ws, st, flags_zeroed);
+    case 512: return run_compact<512>(d, K, V, fr, pa, n, keep, budget, ws, st, flags_zeroed);
+    case 1024: return run_compact<1024>(d, K, V, fr, pa, n, keep, budget, ws, st, flags_zeroed);
   }
   return IPV_ERR_SHAPE;
 }
@@ -343,14 +352,14 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
   };
   IPV_TRY(mark(0));
   IPV_TRY(scores(d, K, V, frame_idx, patch_idx, n_tokens, recent_frames, tar, van, ws, st,
-                 [&]() { return mark(1); }));
+                 [&]() { return mark(1); }, compact_chunks(budget)));
   IPV_TRY(mark(2));
   if (cv_tau) IPV_TRY(pool_d(d, cv_tau, van, frame_idx, patch_idx, n_tokens, nullptr, ws, st));
   IPV_TRY(mark(3));
   IPV_TRY(select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
                  err_word(ws), st));
   IPV_TRY(mark(4));
-  IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, st));
+  IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, st, true));
   return mark(5);
 }
 

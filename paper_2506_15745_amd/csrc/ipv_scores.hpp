@@ -148,16 +148,23 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
   }
 }
 
+// zero (optional): the first block of each slice also zeroes zero_per_slice
+// words at zero + slice * zero_per_slice (the compaction flags of a pass,
+// saving a launch).
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
                                                       const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
                                                       int32_t r, int32_t p, int32_t blocks_per_slice,
                                                       float* __restrict__ table, int32_t* __restrict__ first_recent,
-                                                      uint32_t* err) {
+                                                      uint32_t* err, uint32_t* __restrict__ zero,
+                                                      int32_t zero_per_slice) {
   constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
   extern __shared__ int32_t slot[];
-  table_block<T, D, 256>(K, frame_idx, patch_idx, S, n, r, p, blockIdx.x / blocks_per_slice,
-                         (int32_t)(blockIdx.x % blocks_per_slice) * GROUPS, table, first_recent, err, slot);
+  const int64_t slice = blockIdx.x / blocks_per_slice;
+  const int32_t q0 = (int32_t)(blockIdx.x % blocks_per_slice) * GROUPS;
+  if (zero && q0 == 0)
+    for (int i = threadIdx.x; i < zero_per_slice; i += 256) zero[slice * zero_per_slice + i] = 0u;
+  table_block<T, D, 256>(K, frame_idx, patch_idx, S, n, r, p, slice, q0, table, first_recent, err, slot);
 }
 
 // ---------------------------------------------------------------- fused TaR + VaN sweep
