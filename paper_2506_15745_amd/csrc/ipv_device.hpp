@@ -51,7 +51,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferDword3);
 }
 
-__device__ inline void store16(void* p, const Raw16& v) { *reinterpret_cast<Raw16*>(p) = v; }
+// Nontemporal (streaming) store: compacted rows are not read again in the
+// pass, and storing them this way keeps them from lingering as dirty lines
+// that a later kernel's reads would have to write back first.
+typedef uint32_t U32x4 __attribute__((ext_vector_type(4)));
+__device__ inline void store16(void* p, const Raw16& v) {
+  const U32x4 x = {v.w[0], v.w[1], v.w[2], v.w[3]};
+  __builtin_nontemporal_store(x, reinterpret_cast<U32x4*>(p));
+}
 
 // ---- cross-lane moves
 // DPP moves run in the vector ALU; __shfl_* goes through the LDS crossbar
