@@ -2,67 +2,174 @@
 // NT threads per (stream, layer, head) slice.
 //
 // Thread t owns the RPT consecutive rows [t*RPT, (t+1)*RPT). All of its frame
-// ids and both score columns are loaded at once (16-byte loads), turned into
-// order-preserving 32-bit keys (-0.0 equal to +0.0) and kept in registers.
+// ids and both score columns are loaded at once (16-byte buffer loads),
+// turned into order-preserving 32-bit keys (-0.0 equal to +0.0) and kept in
+// registers.
 //
 // Each stage picks the top k of its candidates with an MSB-first radix
 // select over the keys: 8-bit digits starting below the bits that all the
-// candidates share, an LDS histogram per digit (two buffers, alternating, so
-// a digit costs two barriers), stopping as soon as the threshold bin holds
-// exactly the keys still needed. Keys above the threshold prefix are in;
-// among keys equal to it, an exclusive scan of per-thread counts in row order
-// lets the lowest row indices in first. That is exactly "higher score first,
-// then lower row index".
+// candidates share, an LDS histogram per digit, stopping as soon as the
+// threshold bin holds exactly the keys still needed. Keys above the threshold
+// prefix are in; if the bits run out first, the keys equal to it go to the
+// lowest row indices (an exclusive scan of per-thread counts in row order).
+// That is exactly "higher score first, then lower row index".
+//
+// Latency is set by the number of workgroup barriers, so:
+//   * the block-wide minimum and maximum of both stages' keys come out of the
+//     barrier that also publishes the window start (the VaN range is taken
+//     over all past rows, a superset of its candidates, which still bounds
+//     their common prefix);
+//   * a digit costs one barrier: after it, every wave reads the whole
+//     histogram and finds the threshold digit itself (the same answer in all
+//     waves). Histograms rotate over three LDS buffers, so a buffer is
+//     cleared only after the barrier that follows its last reader;
+//   * each histogram has kHistCopies copies, lane l adding into copy
+//     l % kHistCopies, so lanes of one wave that hit the same bin mostly hit
+//     different words in different banks;
+//   * scans take one barrier: each wave adds up the wave totals it needs.
 #pragma once
 
 #include "ipv_device.hpp"
 
 namespace ipv {
 
+// A histogram is kHistCopies copies of 256 bins, copy-major with a skew of
+// kHistSkew words so that the copies of one bin sit in different LDS banks:
+// word copy * kHistStride + bin.
+constexpr int kHistCopies = 4;
+constexpr int kHistSkew = 4;
+constexpr int kHistStride = 256 + kHistSkew;
+constexpr int kHistWords = kHistCopies * kHistStride;
+
 template <int NT>
 struct SelShared {
   static constexpr int NW = NT / kWave;
-  uint32_t hist[2][256];
-  int32_t wave_tot[NW];
-  int32_t wave_off[NW];
-  uint32_t wave_min[NW], wave_max[NW];
-  int32_t total;
-  int32_t digit;
-  int32_t above;
-  int32_t done;
+  alignas(16) uint32_t hist[3][kHistWords];
+  uint32_t wave_min[2][NW], wave_max[2][NW];  // [TaR, VaN] key ranges per wave
+  uint32_t late_min[NW], late_max[NW];        // VaN range when its keys load late
+  uint32_t wave_bad[NW];
+  int32_t wave_tot[3][NW];                    // [TaR ties, VaN ties, output positions]
   int32_t first_recent;
-  int32_t bad;
 };
 
-// Exclusive prefix sum over the workgroup in thread order; *total gets the sum.
+// Exclusive prefix sum over the workgroup in thread order (one barrier);
+// *total gets the sum. `tot` is used by this scan only.
 template <int NT>
-__device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, SelShared<NT>& sh, int32_t* total) {
+__device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t* tot, int32_t* total) {
   constexpr int NW = NT / kWave;
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int32_t incl = wave_inclusive_scan(v);
-  if (lane == kWave - 1) sh.wave_tot[w] = incl;
+  if (lane == kWave - 1) tot[w] = incl;
   __syncthreads();
-  if (w == 0) {
-    const int32_t t = lane < NW ? sh.wave_tot[lane] : 0;
-    const int32_t ti = wave_inclusive_scan(t);
-    if (lane < NW) sh.wave_off[lane] = ti - t;
-    if (lane == NW - 1) sh.total = ti;
+  int32_t off = 0, sum = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const int32_t t = tot[i];
+    off += i < w ? t : 0;
+    sum += t;
   }
-  __syncthreads();
-  const int32_t res = incl - v + sh.wave_off[w];
-  *total = sh.total;
-  __syncthreads();
-  return res;
+  *total = sum;
+  return incl - v + off;
 }
 
-// Top-k of the candidate rows (bits of `cand`) by key; returns this thread's
-// picks. 0 < k <= number of candidates.
+// State of one stage's digit loop, the same in every thread.
+struct Radix {
+  uint32_t prefix, pmask;
+  int32_t remaining;
+  bool done;
+};
+
+// The digit loop for the top k of `cand` keys whose common bits are those of
+// [mn, mx]. `buf` is the rotating histogram counter (shared by both stages).
 template <int NT, int RPT>
-__device__ __forceinline__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64_t cand, int32_t k, SelShared<NT>& sh) {
+__device__ __forceinline__ Radix radix_digits(const uint32_t (&key)[RPT], uint64_t cand, int32_t k, uint32_t mn,
+                                              uint32_t mx, SelShared<NT>& sh, int& buf) {
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int common = (mn == mx) ? 32 : __clz((int)(mn ^ mx));
+  Radix R;
+  R.pmask = common == 0 ? 0u : (common == 32 ? 0xffffffffu : 0xffffffffu << (32 - common));
+  R.prefix = mn & R.pmask;
+  R.remaining = k;
+  R.done = false;
+  const int copy = lane % kHistCopies;
+#pragma unroll 1
+  for (int top = 32 - common; top > 0 && !R.done; top -= 8) {
+    const int shift = max(0, top - 8);
+    const uint32_t dmask = (1u << (top - shift)) - 1u;
+    uint32_t* h = sh.hist[buf];
+#pragma unroll
+    for (int i = 0; i < RPT; ++i)
+      if (((cand >> i) & 1ull) && (key[i] & R.pmask) == R.prefix)
+        atomicAdd(&h[copy * kHistStride + ((key[i] >> shift) & dmask)], 1u);
+    // the next digit's buffer, last read two digits ago
+    uint32_t* nxt = sh.hist[buf == 2 ? 0 : buf + 1];
+    for (int i = tid; i < kHistWords; i += NT) nxt[i] = 0u;
+    __syncthreads();
+    // every wave: lane l holds digits 255-4l .. 252-4l (descending digit order),
+    // read as one 16-byte run of bins 252-4l .. 255-4l per copy
+    int32_t c[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int cp = 0; cp < kHistCopies; ++cp) {
+      const uint4 v = *reinterpret_cast<const uint4*>(h + cp * kHistStride + 252 - 4 * lane);
+      c[0] += (int32_t)v.w;
+      c[1] += (int32_t)v.z;
+      c[2] += (int32_t)v.y;
+      c[3] += (int32_t)v.x;
+    }
+    const int32_t s = c[0] + c[1] + c[2] + c[3];
+    const int32_t incl = wave_inclusive_scan(s);
+    const int32_t excl = incl - s;
+    const uint64_t hit = __ballot(excl < R.remaining && R.remaining <= incl);
+    const int L = __ffsll((unsigned long long)hit) - 1;  // the lane holding the threshold digit
+    int32_t above = excl, j = 0;
+    while (j < 3 && above + c[j] < R.remaining) above += c[j++];
+    const int32_t digit = 255 - 4 * lane - j;
+    const int32_t bin = j == 0 ? c[0] : (j == 1 ? c[1] : (j == 2 ? c[2] : c[3]));
+    const int32_t d = __builtin_amdgcn_readlane(digit, L);
+    const int32_t a = __builtin_amdgcn_readlane(above, L);
+    const int32_t cnt = __builtin_amdgcn_readlane(bin, L);
+    R.remaining -= a;
+    R.prefix |= (uint32_t)d << shift;
+    R.pmask |= dmask << shift;
+    R.done = cnt == R.remaining;  // the threshold bin is taken whole
+    buf = buf == 2 ? 0 : buf + 1;
+  }
+  return R;
+}
+
+// This thread's picks among `cand` after the digit loop. Ties on the full
+// key (the loop ran out of bits) go to the lowest rows.
+template <int NT, int RPT>
+__device__ __forceinline__ uint64_t radix_picks(const uint32_t (&key)[RPT], uint64_t cand, const Radix& R,
+                                                int32_t* tie_tot) {
+  uint64_t pick = 0, eq = 0;
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    if (!((cand >> i) & 1ull)) continue;
+    const uint32_t mk = key[i] & R.pmask;
+    if (mk > R.prefix) pick |= 1ull << i;
+    if (mk == R.prefix) eq |= 1ull << i;
+  }
+  if (R.done) return pick | eq;
+  int32_t tot;
+  int32_t taken = block_exclusive_scan<NT>(__popcll(eq), tie_tot, &tot);
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+    if ((eq >> i) & 1ull) {
+      if (taken < R.remaining) pick |= 1ull << i;
+      ++taken;
+    }
+  return pick;
+}
+
+// Block-wide min and max of this thread's candidate keys (one barrier).
+template <int NT, int RPT>
+__device__ __forceinline__ void block_min_max(const uint32_t (&key)[RPT], uint64_t cand, SelShared<NT>& sh,
+                                              uint32_t& mn, uint32_t& mx) {
   constexpr int NW = NT / kWave;
-  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
-  // bits shared by every candidate key
-  uint32_t mn = 0xffffffffu, mx = 0u;
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  mn = 0xffffffffu;
+  mx = 0u;
 #pragma unroll
   for (int i = 0; i < RPT; ++i)
     if ((cand >> i) & 1ull) {
@@ -71,76 +178,15 @@ __device__ __forceinline__ uint64_t radix_top(const uint32_t (&key)[RPT], uint64
     }
   wave_min_max(mn, mx);
   if (lane == 0) {
-    sh.wave_min[w] = mn;
-    sh.wave_max[w] = mx;
+    sh.late_min[w] = mn;
+    sh.late_max[w] = mx;
   }
-  if (tid < 256) sh.hist[0][tid] = 0u;
   __syncthreads();
-  mn = sh.wave_min[0];
-  mx = sh.wave_max[0];
 #pragma unroll
-  for (int i = 1; i < NW; ++i) {
-    mn = min(mn, sh.wave_min[i]);
-    mx = max(mx, sh.wave_max[i]);
+  for (int i = 0; i < NW; ++i) {
+    mn = min(mn, sh.late_min[i]);
+    mx = max(mx, sh.late_max[i]);
   }
-  const int common = (mn == mx) ? 32 : __clz((int)(mn ^ mx));
-  uint32_t pmask = common == 0 ? 0u : (common == 32 ? 0xffffffffu : 0xffffffffu << (32 - common));
-  uint32_t prefix = mn & pmask;
-  int32_t remaining = k;
-  int cur = 0;
-#pragma unroll 1
-  for (int top = 32 - common; top > 0; top -= 8) {
-    const int shift = max(0, top - 8);
-    const uint32_t dmask = (1u << (top - shift)) - 1u;
-#pragma unroll
-    for (int i = 0; i < RPT; ++i)
-      if (((cand >> i) & 1ull) && (key[i] & pmask) == prefix) atomicAdd(&sh.hist[cur][(key[i] >> shift) & dmask], 1u);
-    if (tid < 256) sh.hist[cur ^ 1][tid] = 0u;  // the next digit's buffer
-    __syncthreads();
-    if (w == 0) {
-      // lane l holds digits 255-4l .. 252-4l: lane order is descending digit order
-      int32_t c[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) c[j] = (int32_t)sh.hist[cur][255 - 4 * lane - j];
-      const int32_t s = c[0] + c[1] + c[2] + c[3];
-      const int32_t incl = wave_inclusive_scan(s);
-      const int32_t excl = incl - s;
-      if (excl < remaining && remaining <= incl) {
-        int32_t above = excl;
-        int j = 0;
-        while (above + c[j] < remaining) above += c[j++];
-        sh.digit = 255 - 4 * lane - j;
-        sh.above = above;
-        sh.done = (above + c[j] == remaining);  // the threshold bin is taken whole
-      }
-    }
-    __syncthreads();
-    remaining -= sh.above;
-    prefix |= (uint32_t)sh.digit << shift;
-    pmask |= dmask << shift;
-    cur ^= 1;
-    if (sh.done) break;
-  }
-  // masked keys above the prefix are in; `remaining` of those equal to it go
-  // to the lowest rows (all of them when the loop stopped early)
-  int32_t eq = 0;
-#pragma unroll
-  for (int i = 0; i < RPT; ++i) eq += ((cand >> i) & 1ull) && (key[i] & pmask) == prefix;
-  int32_t tot;
-  int32_t taken = block_exclusive_scan<NT>(eq, sh, &tot);
-  uint64_t pick = 0;
-#pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    if (!((cand >> i) & 1ull)) continue;
-    const uint32_t mk = key[i] & pmask;
-    if (mk > prefix) {
-      pick |= 1ull << i;
-    } else if (mk == prefix) {
-      if (taken < remaining) pick |= 1ull << i;
-      ++taken;
-    }
-  }
-  return pick;
 }
 
 // Rows [row0, row0 + RPT) of one slice's column (S rows of 4 bytes); rows at
@@ -172,7 +218,8 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
                              const int32_t* __restrict__ frame_idx, int64_t S, int32_t n, int32_t budget,
                              int32_t tar_total, int32_t r, int32_t* __restrict__ keep_idx,
                              uint32_t* err, int64_t slice, SelShared<NT>& sh) {
-  const int tid = threadIdx.x;
+  constexpr int NW = NT / kWave;
+  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int64_t base = slice * S;
   const int64_t row0 = (int64_t)tid * RPT;
   int32_t* keep = keep_idx + slice * budget;
@@ -189,11 +236,7 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   const int32_t prev_row = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)max(row0 - 1, (int64_t)0) * 4u,
                                                                           0, 0);
   const int32_t before = row0 > 0 ? prev_row : INT32_MIN;
-  if (tid == 0) {
-    sh.first_recent = n;
-    sh.bad = 0;
-  }
-  __syncthreads();
+  for (int i = tid; i < kHistWords; i += NT) sh.hist[0][i] = 0u;
 
   const int64_t thr = (int64_t)last - r + 1;
   uint64_t valid = 0, recent = 0;
@@ -206,7 +249,10 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
       valid |= 1ull << i;
       const bool rec = (int64_t)f >= thr;
       if (rec) recent |= 1ull << i;
-      if (rec && (int64_t)prev < thr) sh.first_recent = (int32_t)(row0 + i);  // the window's first row
+      // the window's first row: with any frame ids, at least one row has a
+      // recent frame and a non-recent predecessor (or is row 0); with
+      // non-decreasing ids exactly one
+      if (rec && (int64_t)prev < thr) sh.first_recent = (int32_t)(row0 + i);
       bad |= f < prev;
       prev = f;
       nan_t |= !rec && __uint_as_float(kt[i]) != __uint_as_float(kt[i]);
@@ -215,45 +261,79 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
     kt[i] = order_key(__uint_as_float(kt[i]));
     if (kEarlyVan) kv[i] = order_key(__uint_as_float(kv[i]));
   }
-  if (bad) sh.bad = 1;
+  const uint64_t past = valid & ~recent;
+  // key ranges of both stages over the past rows, and the frame check
+  uint32_t tmn = 0xffffffffu, tmx = 0u, vmn = 0xffffffffu, vmx = 0u;
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+    if ((past >> i) & 1ull) {
+      tmn = min(tmn, kt[i]);
+      tmx = max(tmx, kt[i]);
+      if (kEarlyVan) {
+        vmn = min(vmn, kv[i]);
+        vmx = max(vmx, kv[i]);
+      }
+    }
+  wave_min_max(tmn, tmx);
+  if (kEarlyVan) wave_min_max(vmn, vmx);
+  const bool wbad = __ballot(bad) != 0;
+  if (lane == 0) {
+    sh.wave_min[0][w] = tmn;
+    sh.wave_max[0][w] = tmx;
+    sh.wave_min[1][w] = vmn;
+    sh.wave_max[1][w] = vmx;
+    sh.wave_bad[w] = wbad;
+  }
   __syncthreads();
+  bool any_bad = false;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    tmn = min(tmn, sh.wave_min[0][i]);
+    tmx = max(tmx, sh.wave_max[0][i]);
+    vmn = min(vmn, sh.wave_min[1][i]);
+    vmx = max(vmx, sh.wave_max[1][i]);
+    any_bad |= sh.wave_bad[i] != 0;
+  }
   // with non-decreasing frame ids the window is the suffix starting at first_recent
   const int32_t n_recent = n - sh.first_recent;
-  const bool broken = sh.bad || n_recent > budget;
+  const bool broken = any_bad || n_recent > budget;
   if (broken) {
     // metadata breaks the cache invariants: report, and keep rows 0..C-1 in place
-    if (tid == 0) raise_error(err, sh.bad ? 2u : 4u);
+    if (tid == 0) raise_error(err, any_bad ? 2u : 4u);
     for (int32_t j = tid; j < budget; j += NT) keep[j] = j;
-  } else {
-    const int32_t b_tar = max(0, tar_total - n_recent);
-    const int32_t b_van = budget - n_recent - b_tar;
-    const uint64_t past = valid & ~recent;
-    uint64_t pick_t = 0, pick_v = 0;
-    if (b_tar > 0) {
-      if (nan_t) raise_error(err, 16u);
-      pick_t = radix_top<NT, RPT>(kt, past, b_tar, sh);
-    }
-    if (b_van > 0) {
-      if (!kEarlyVan) {
-        load_row_run<RPT, VEC>(van + base, S, row0, kv);
-#pragma unroll
-        for (int i = 0; i < RPT; ++i) {
-          nan_v |= ((past >> i) & 1ull) && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
-          kv[i] = order_key(__uint_as_float(kv[i]));
-        }
-      }
-      if (nan_v) raise_error(err, 16u);
-      pick_v = radix_top<NT, RPT>(kv, past & ~pick_t, b_van, sh);
-    }
-    const uint64_t kept = recent | pick_t | pick_v;
-    int32_t total;
-    int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh, &total);
-    if (total != budget && tid == 0) raise_error(err, 16u);  // only reachable with NaN keys
-#pragma unroll
-    for (int i = 0; i < RPT; ++i)
-      if (((kept >> i) & 1ull) && pos < budget) keep[pos++] = (int32_t)(row0 + i);
+    return;
   }
-  __syncthreads();  // the caller may reuse sh
+  const int32_t b_tar = max(0, tar_total - n_recent);
+  const int32_t b_van = budget - n_recent - b_tar;
+  uint64_t pick_t = 0, pick_v = 0;
+  int buf = 0;
+  if (b_tar > 0) {
+    if (nan_t) raise_error(err, 16u);
+    const Radix R = radix_digits<NT, RPT>(kt, past, b_tar, tmn, tmx, sh, buf);
+    pick_t = radix_picks<NT, RPT>(kt, past, R, sh.wave_tot[0]);
+  }
+  if (b_van > 0) {
+    const uint64_t cand = past & ~pick_t;
+    if (!kEarlyVan) {
+      load_row_run<RPT, VEC>(van + base, S, row0, kv);
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        nan_v |= ((past >> i) & 1ull) && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
+        kv[i] = order_key(__uint_as_float(kv[i]));
+      }
+      block_min_max<NT, RPT>(kv, cand, sh, vmn, vmx);
+    }
+    if (nan_v) raise_error(err, 16u);
+    const Radix R = radix_digits<NT, RPT>(kv, cand, b_van, vmn, vmx, sh, buf);
+    pick_v = radix_picks<NT, RPT>(kv, cand, R, sh.wave_tot[1]);
+  }
+  const uint64_t kept = recent | pick_t | pick_v;
+  int32_t total;
+  int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh.wave_tot[2], &total);
+  if (total != budget && tid == 0) raise_error(err, 16u);  // only reachable with NaN keys
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+    if (((kept >> i) & 1ull) && pos < budget) keep[pos++] = (int32_t)(row0 + i);
 }
 
 template <int NT, int RPT, bool VEC>
