@@ -72,7 +72,12 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
   const int32_t* keep = keep_idx + slice * budget;
   const bool data = part < 2 * C::NCB;
 
-  // 1. loads
+  // 1. loads: first every keep index of the chunk, then every source row,
+  // each batch issued at once. Buffer loads need no branches: a lane with
+  // nothing to load reads past the end of the resource, which returns zeros
+  // without touching memory.
+  constexpr uint32_t kSkip = 0xfffffff0u;
+  const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(keep, (uint32_t)budget * 4u);
   Raw16 buf[U];
   int32_t src[U];
   int32_t mval = 0, msrc = -1;
@@ -80,34 +85,39 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
   char* base = nullptr;
   int32_t* marr = nullptr;
   const int sub = tid / LPP, lane = tid % LPP;
+  const uint32_t col = (uint32_t)((part % C::NCB) * C::CB + lane * 16);  // byte offset in a row
   if (data) {
-    base = (part < C::NCB ? K : V) + slice * S * RB + (part % C::NCB) * C::CB;
+    base = (part < C::NCB ? K : V) + slice * S * RB;
+    const __amdgpu_buffer_rsrc_t drs = buffer_rsrc(base, (uint32_t)(S * RB));
+    int32_t kj[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t j = c0 + u * RPS + sub;
-      src[u] = -1;
-      if (j < c1) {
-        const int32_t s = keep[j];
-        if (s < j || s >= n) {
-          bad = true;
-        } else if (s != j) {
-          src[u] = s;
-          buf[u] = load16(base + (int64_t)s * RB + lane * 16);
-        }
-      }
+      kj[u] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(krs, j < c1 ? (uint32_t)j * 4u : kSkip, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = c0 + u * RPS + sub;
+      const int32_t s = kj[u];
+      const bool in = j < c1;
+      bad |= in && (s < j || s >= n);
+      src[u] = (in && s > j && s < n) ? s : -1;
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(drs, src[u] >= 0 ? (uint32_t)src[u] * RB + col : kSkip, 0, 0);
+      buf[u].w[0] = v[0];
+      buf[u].w[1] = v[1];
+      buf[u].w[2] = v[2];
+      buf[u].w[3] = v[3];
     }
   } else {
-    marr = (tid < CH ? frame_idx : patch_idx) + slice * S;
+    // CH is a multiple of the wave size: the array is uniform per wave
+    marr = (__builtin_amdgcn_readfirstlane(tid) < CH ? frame_idx : patch_idx) + slice * S;
+    const __amdgpu_buffer_rsrc_t mrs = buffer_rsrc(marr, (uint32_t)(S * 4));
     const int64_t j = c0 + (tid % CH);
-    if (j < c1) {
-      const int32_t s = keep[j];
-      if (s < j || s >= n) {
-        bad = true;
-      } else if (s != j) {
-        msrc = s;
-        mval = marr[s];
-      }
-    }
+    const bool in = j < c1;
+    const int32_t s = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(krs, in ? (uint32_t)j * 4u : kSkip, 0, 0);
+    bad = in && (s < j || s >= n);
+    msrc = (in && s > j && s < n) ? s : -1;
+    mval = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(mrs, msrc >= 0 ? (uint32_t)msrc * 4u : kSkip, 0, 0);
   }
   if (bad) raise_error(err, 8u);
   // Use every loaded register in an opaque statement: the compiler must wait
@@ -151,7 +161,7 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
     if (data) {
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        if (src[u] >= 0) store16(base + (c0 + u * RPS + sub) * RB + lane * 16, buf[u]);
+        if (src[u] >= 0) store16(base + (c0 + u * RPS + sub) * RB + col, buf[u]);
     } else if (msrc >= 0) {
       marr[c0 + (tid % CH)] = mval;
     }
