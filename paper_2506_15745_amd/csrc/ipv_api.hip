@@ -24,8 +24,9 @@ namespace {
 constexpr int32_t kMaxRows = 65536;  // select: 1024 threads x 64 row flags
 constexpr int64_t kMaxWindowRows = 65536;        // r * p: recent rows scanned per table block
 constexpr int32_t kMaxRecentFrames = 256;
-constexpr int kCompactThreads = 256;
-constexpr int kMinChunkRows = kCompactThreads / 2;  // smallest compaction chunk of any kernel
+constexpr int kCompactThreads = 512;
+constexpr int kCompactRows = 256;      // rows per compaction chunk
+constexpr int kCompactColBytes = 256;  // largest column block a compaction walk copies
 
 struct Dims {
   int64_t B, L, H, S, D, p, slices;
@@ -82,8 +83,8 @@ ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
 // pool   B * L             int32 pooling window per (stream, layer)
 // flags  walks * chunks    uint32 per compaction chunk (1 once its rows are loaded)
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
-int64_t compact_parts(const Dims& d) { return 2 * std::max<int64_t>(1, d.D * d.elem / 128) + 1; }
-int64_t max_chunks(const Dims& d) { return (d.S + kMinChunkRows - 1) / kMinChunkRows; }
+int64_t compact_parts(const Dims& d) { return 2 * std::max<int64_t>(1, d.D * d.elem / kCompactColBytes) + 1; }
+int64_t max_chunks(const Dims& d) { return (d.S + kCompactRows - 1) / kCompactRows; }
 size_t table_offset() { return kWsHeader; }
 size_t table_bytes(const Dims& d) { return (size_t)(d.slices * d.p * d.D) * sizeof(float); }
 size_t first_offset(const Dims& d) { return up256(table_offset() + table_bytes(d)); }
@@ -210,19 +211,18 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
   return run_select<64>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
 }
 
-int64_t compact_chunks(int32_t budget) { return (budget + kMinChunkRows - 1) / kMinChunkRows; }
+int64_t compact_chunks(int32_t budget) { return (budget + kCompactRows - 1) / kCompactRows; }
 
 // flags_zeroed: the pass's table kernel has zeroed the flags already
 template <int RB>
 ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
                        int32_t budget, void* ws, hipStream_t st, bool flags_zeroed) {
-  using C = CompactCfg<RB, kCompactThreads>;
-  static_assert(C::CH == kMinChunkRows, "chunk rows");
+  using C = CompactCfg<RB, kCompactThreads, kCompactRows, kCompactColBytes>;
   const uint32_t chunks = (uint32_t)compact_chunks(budget);
   const int64_t total = d.slices * C::PARTS * chunks;
   if (!flags_zeroed)
     k_clear_flags<<<dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), total);
-  k_compact<RB, kCompactThreads><<<dim3((uint32_t)total), dim3(kCompactThreads), 0, st>>>(
+  k_compact<RB, kCompactThreads, kCompactRows, kCompactColBytes><<<dim3((uint32_t)total), dim3(kCompactThreads), 0, st>>>(
       static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
       chunks);
   return launched();

@@ -1,10 +1,10 @@
 // In-place, order-preserving compaction (Sec. 3.1; Algorithm 1 step (5)):
 // row j <- row keep[j] for j < C, for K, V, frame_idx and patch_idx.
 //
-// The rows of a slice form independent "walks": each 128-byte column block of
-// K, each of V, and the metadata pair. A walk's output rows are cut into
-// chunks of CH rows and every chunk is one workgroup (CH = half the
-// workgroup size), so the whole copy runs
+// The rows of a slice form independent "walks": each column block of K (up
+// to CBMAX bytes of every row), each of V, and the metadata pair. A walk's
+// output rows are cut into chunks of CH rows and every chunk is one
+// workgroup, so the whole copy runs
 // in parallel. The in-place hazard: a chunk writes rows [c0, c1) that an
 // earlier chunk of the same walk may still have to read (keep[j] >= j, so a
 // chunk's sources lie at or after its own rows, never before). Hence:
@@ -22,7 +22,8 @@
 // and does not store.
 //
 // The flags (one uint32 per chunk, in the workspace) must be zero when the
-// kernel starts; k_clear_flags (or the selection kernel) zeroes them.
+// kernel starts; k_clear_flags (or, in a full pass, the table kernel) zeroes
+// them.
 #pragma once
 
 #include "ipv_device.hpp"
@@ -31,16 +32,19 @@ namespace ipv {
 
 constexpr uint32_t kSpinLimit = 1u << 20;
 
-template <int RB, int NT>  // bytes per row, threads per chunk
+// bytes per row, threads per chunk, rows per chunk, largest column block
+template <int RB, int NT, int CHR, int CBMAX>
 struct CompactCfg {
-  static constexpr int CH = NT / 2;               // rows per chunk (the metadata walk: 2 arrays x CH rows)
-  static constexpr int CB = RB < 128 ? RB : 128;  // bytes per column block (one cache line)
-  static constexpr int NCB = RB / CB;             // column blocks per row
-  static constexpr int LPP = CB / 16;             // lanes per row piece
-  static constexpr int RPS = NT / LPP;            // rows per step
-  static constexpr int U = CH / RPS;              // steps per chunk
-  static constexpr int PARTS = 2 * NCB + 1;       // walks per slice: K blocks, V blocks, metadata
+  static constexpr int CH = CHR;                      // rows per chunk
+  static constexpr int CB = RB < CBMAX ? RB : CBMAX;  // bytes per column block
+  static constexpr int NCB = RB / CB;                 // column blocks per row
+  static constexpr int LPP = CB / 16;                 // lanes per row piece
+  static constexpr int RPS = NT / LPP;                // rows per step
+  static constexpr int U = CH / RPS;                  // steps per chunk
+  static constexpr int MPT = 2 * CH / NT;             // metadata walk: 2 arrays x CH rows over NT threads
+  static constexpr int PARTS = 2 * NCB + 1;           // walks per slice: K blocks, V blocks, metadata
   static_assert(U >= 1 && U * RPS == CH, "chunk shape");
+  static_assert(MPT >= 1 && MPT * NT == 2 * CH && CH % kWave == 0, "metadata walk shape");
 };
 
 __device__ inline uint32_t load_flag(const uint32_t* p) {
@@ -59,13 +63,13 @@ __global__ void k_clear_flags(uint32_t* flags, int64_t count) {
 
 // Chunk k of walk `part` of `slice` with NT threads. wflags: the walk's flags
 // (one per chunk, zero at kernel start). ok_sh: one word of LDS.
-template <int RB, int NT>
+template <int RB, int NT, int CHR, int CBMAX>
 __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __restrict__ V, int32_t* __restrict__ frame_idx,
                               int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t budget,
                               const int32_t* __restrict__ keep_idx, uint32_t* err, uint32_t* wflags,
                               int64_t slice, int part, uint32_t k, uint32_t* ok_sh) {
-  using C = CompactCfg<RB, NT>;
-  constexpr int LPP = C::LPP, RPS = C::RPS, U = C::U, CH = C::CH;
+  using C = CompactCfg<RB, NT, CHR, CBMAX>;
+  constexpr int LPP = C::LPP, RPS = C::RPS, U = C::U, CH = C::CH, MPT = C::MPT;
   const int tid = threadIdx.x;
   const int64_t c0 = (int64_t)k * CH;
   const int64_t c1 = min((int64_t)budget, c0 + CH);
@@ -80,10 +84,9 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
   const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(keep, (uint32_t)budget * 4u);
   Raw16 buf[U];
   int32_t src[U];
-  int32_t mval = 0, msrc = -1;
+  int32_t mval[MPT], msrc[MPT];
   bool bad = false;
   char* base = nullptr;
-  int32_t* marr = nullptr;
   const int sub = tid / LPP, lane = tid % LPP;
   const uint32_t col = (uint32_t)((part % C::NCB) * C::CB + lane * 16);  // byte offset in a row
   if (data) {
@@ -109,15 +112,25 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
       buf[u].w[3] = v[3];
     }
   } else {
-    // CH is a multiple of the wave size: the array is uniform per wave
-    marr = (__builtin_amdgcn_readfirstlane(tid) < CH ? frame_idx : patch_idx) + slice * S;
-    const __amdgpu_buffer_rsrc_t mrs = buffer_rsrc(marr, (uint32_t)(S * 4));
-    const int64_t j = c0 + (tid % CH);
-    const bool in = j < c1;
-    const int32_t s = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(krs, in ? (uint32_t)j * 4u : kSkip, 0, 0);
-    bad = in && (s < j || s >= n);
-    msrc = (in && s > j && s < n) ? s : -1;
-    mval = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(mrs, msrc >= 0 ? (uint32_t)msrc * 4u : kSkip, 0, 0);
+    // element e = tid + i * NT: array e / CH (frame ids, patch ids), row e % CH;
+    // CH is a multiple of the wave size, so the array is uniform per wave
+    int32_t kj[MPT];
+#pragma unroll
+    for (int i = 0; i < MPT; ++i) {
+      const int64_t j = c0 + (tid + i * NT) % CH;
+      kj[i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(krs, j < c1 ? (uint32_t)j * 4u : kSkip, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < MPT; ++i) {
+      const int e = __builtin_amdgcn_readfirstlane(tid + i * NT);
+      const __amdgpu_buffer_rsrc_t mrs = buffer_rsrc((e < CH ? frame_idx : patch_idx) + slice * S, (uint32_t)(S * 4));
+      const int64_t j = c0 + (tid + i * NT) % CH;
+      const bool in = j < c1;
+      const int32_t s = kj[i];
+      bad |= in && (s < j || s >= n);
+      msrc[i] = (in && s > j && s < n) ? s : -1;
+      mval[i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(mrs, msrc[i] >= 0 ? (uint32_t)msrc[i] * 4u : kSkip, 0, 0);
+    }
   }
   if (bad) raise_error(err, 8u);
   // Use every loaded register in an opaque statement: the compiler must wait
@@ -125,7 +138,8 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
   // wave's loads of this chunk have landed.
 #pragma unroll
   for (int u = 0; u < U; ++u) asm volatile("" ::"v"(buf[u].w[0]));
-  asm volatile("" ::"v"(mval));
+#pragma unroll
+  for (int i = 0; i < MPT; ++i) asm volatile("" ::"v"(mval[i]));
   __syncthreads();
 
   // 2. publish
@@ -162,8 +176,12 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if (src[u] >= 0) store16(base + (c0 + u * RPS + sub) * RB + col, buf[u]);
-    } else if (msrc >= 0) {
-      marr[c0 + (tid % CH)] = mval;
+    } else {
+#pragma unroll
+      for (int i = 0; i < MPT; ++i) {
+        const int e = tid + i * NT;
+        if (msrc[i] >= 0) ((e < CH ? frame_idx : patch_idx) + slice * S)[c0 + e % CH] = mval[i];
+      }
     }
   } else if (tid == 0) {
     raise_error(err, 32u);
@@ -171,17 +189,17 @@ __device__ __forceinline__ void compact_chunk(char* __restrict__ K, char* __rest
 }
 
 // grid: slices * PARTS * n_chunks workgroups of NT threads, id = chunk * walks + walk
-template <int RB, int NT>
+template <int RB, int NT, int CHR, int CBMAX>
 __global__ __launch_bounds__(NT) void k_compact(char* __restrict__ K, char* __restrict__ V,
                                                 int32_t* __restrict__ frame_idx, int32_t* __restrict__ patch_idx,
                                                 int64_t S, int32_t n, int32_t budget,
                                                 const int32_t* __restrict__ keep_idx, uint32_t* err,
                                                 uint32_t* flags, uint32_t n_chunks) {
-  using C = CompactCfg<RB, NT>;
+  using C = CompactCfg<RB, NT, CHR, CBMAX>;
   __shared__ uint32_t ok_sh;
   const uint32_t walks = gridDim.x / n_chunks;
   const uint32_t k = blockIdx.x / walks, w = blockIdx.x % walks;
-  compact_chunk<RB, NT>(K, V, frame_idx, patch_idx, S, n, budget, keep_idx, err, flags + (int64_t)w * n_chunks,
+  compact_chunk<RB, NT, CHR, CBMAX>(K, V, frame_idx, patch_idx, S, n, budget, keep_idx, err, flags + (int64_t)w * n_chunks,
                         w / C::PARTS, (int)(w % C::PARTS), k, &ok_sh);
 }
 
