@@ -207,25 +207,61 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
   if (!TAR) rec = n;
   const float* mtab = table + (int64_t)slice * p * D + lane * EPL;
 
+  // Every load is a buffer load issued without a branch (a lane with nothing
+  // to read uses an offset past the end and gets zeros); the patch ids of
+  // the column's U rows come from one load per lane: lane l reads row l % 4,
+  // and a DPP broadcast inside each quad hands row u's id to every lane.
+  static_assert(U == 4 && LPR % 4 == 0, "patch-id broadcast over quads");
+  constexpr uint32_t kSkip = 0xfffffff0u;
+  constexpr uint32_t RB = D * (uint32_t)sizeof(T);
+  const uint32_t lo = (uint32_t)lane * EPL * (uint32_t)sizeof(T);
+  int32_t pq_mine = 0;
+  if (TAR) {
+    const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(patch_idx + base, (uint32_t)(S * 4));
+    const int64_t xm = (int64_t)(f0 + (lane & 3)) * p + col;
+    pq_mine = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, (xm < n && xm < rec) ? (uint32_t)xm * 4u : kSkip,
+                                                            0, 0);
+  }
   Raw16 kr[U], vr[U];
-  int32_t pq[U];
-  float4 ms[EPL / 4];
+  const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(K + base * D, (uint32_t)S * RB);
+  const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(V + base * D, (uint32_t)S * RB);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int64_t x = (int64_t)(f0 + u) * p + col;
-    pq[u] = -1;
-    if (x < n) {
-      if (TAR && x < rec) {
-        pq[u] = patch_idx[base + x];
-        kr[u] = load16(K + (base + x) * D + lane * EPL);
-      }
-      if (VAN) vr[u] = load16(V + (base + x) * D + lane * EPL);
+    if (TAR) {
+      const auto k = __builtin_amdgcn_raw_buffer_load_b128(krs, (x < n && x < rec) ? (uint32_t)x * RB + lo : kSkip, 0, 0);
+      kr[u].w[0] = k[0];
+      kr[u].w[1] = k[1];
+      kr[u].w[2] = k[2];
+      kr[u].w[3] = k[3];
+    }
+    if (VAN) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(vrs, x < n ? (uint32_t)x * RB + lo : kSkip, 0, 0);
+      vr[u].w[0] = v[0];
+      vr[u].w[1] = v[1];
+      vr[u].w[2] = v[2];
+      vr[u].w[3] = v[3];
     }
   }
+  float4 ms[EPL / 4];
   const bool any_past = TAR && (int64_t)f0 * p + col < min(n, rec);
-  if (any_past) {
+  if (TAR) {
+    // the resource base must be uniform: the slice's table, lane offset in the offset
+    const __amdgpu_buffer_rsrc_t mrs = buffer_rsrc(table + (int64_t)slice * p * D, (uint32_t)(p * D * 4));
 #pragma unroll
-    for (int i = 0; i < EPL / 4; ++i) ms[i] = *reinterpret_cast<const float4*>(mtab + (int64_t)col * D + 4 * i);
+    for (int i = 0; i < EPL / 4; ++i) {
+      const auto m = __builtin_amdgcn_raw_buffer_load_b128(
+          mrs, any_past ? (uint32_t)(col * D + lane * EPL + 4 * i) * 4u : kSkip, 0, 0);
+      ms[i] = make_float4(__uint_as_float(m[0]), __uint_as_float(m[1]), __uint_as_float(m[2]),
+                          __uint_as_float(m[3]));
+    }
+  }
+  int32_t pq[U];
+  if (TAR) {
+    pq[0] = (int32_t)dpp_u32<0x00>((uint32_t)pq_mine);
+    pq[1] = (int32_t)dpp_u32<0x55>((uint32_t)pq_mine);
+    pq[2] = (int32_t)dpp_u32<0xAA>((uint32_t)pq_mine);
+    pq[3] = (int32_t)dpp_u32<0xFF>((uint32_t)pq_mine);
   }
   if (VAN) {
 #pragma unroll
