@@ -263,6 +263,10 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
     pq[2] = (int32_t)dpp_u32<0xAA>((uint32_t)pq_mine);
     pq[3] = (int32_t)dpp_u32<0xFF>((uint32_t)pq_mine);
   }
+  // Scores: every lane of a group ends up with all U sums; lane u of the
+  // group stores row u, so a wave stores each score column with one
+  // instruction instead of U.
+  float vsc[U], tsc[U];
   if (VAN) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -274,8 +278,7 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
 #pragma unroll
         for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
       }
-      ss = group_sum<LPR>(ss);
-      if (x < n && lane == 0) van[base + x] = sqrtf(ss);
+      vsc[u] = sqrtf(group_sum<LPR>(ss));
     }
   }
   if (TAR) {
@@ -306,11 +309,16 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
       }
       dot = group_sum<LPR>(dot);
       kk = group_sum<LPR>(kk);
-      if (x < n && lane == 0) {
-        float s = kk > 0.f ? -(dot / sqrtf(kk)) : 0.f;
-        if (s == 0.f) s = 0.f;  // -0.0 -> +0.0
-        tar[base + x] = past ? s : 0.f;
-      }
+      float sc = kk > 0.f ? -(dot / sqrtf(kk)) : 0.f;
+      if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
+      tsc[u] = past ? sc : 0.f;
+    }
+  }
+  if (lane < U) {
+    const int64_t x = (int64_t)(f0 + lane) * p + col;
+    if (x < n) {
+      if (VAN) van[base + x] = lane == 0 ? vsc[0] : lane == 1 ? vsc[1] : lane == 2 ? vsc[2] : vsc[3];
+      if (TAR) tar[base + x] = lane == 0 ? tsc[0] : lane == 1 ? tsc[1] : lane == 2 ? tsc[2] : tsc[3];
     }
   }
 }
