@@ -15,6 +15,8 @@
  *   ipv_compact      in-place, order-preserving gather of the kept rows
  *                    (Sec. 3.1; Algorithm 1 step (5))
  *   ipv_compress     the four steps above, in order, on one stream
+ *   ipv_append       add a frame's rows to the cache (Algorithm 1 step (1))
+ *   ipv_ckv_step     append, then compress when the memory cap is reached
  *
  * ---------------------------------------------------------------- layouts
  * A cache holds B streams x L layers x H KV heads; each (b, l, h) "slice" has
@@ -176,6 +178,38 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
                               int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
                               const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
                               size_t ws_bytes, void* stream, const ipv_events* events);
+
+/*
+ * Append new rows to every slice (Algorithm 1 step (1): the tokens of a new
+ * frame, or part of one, join the cache after prefill). Rows
+ * [n_tokens, n_tokens + rows) of each slice receive K_new / V_new
+ * ([B, L, H, rows, D], same dtype as the cache, device, 16-byte aligned),
+ * frame_idx = frame_id and patch_idx = first_patch + i for the i-th new row.
+ * Needs n_tokens >= 0, rows >= 1, n_tokens + rows <= S and
+ * first_patch + rows <= p. The caller's row count becomes n_tokens + rows.
+ */
+ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                      int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                      int32_t first_patch, void* stream);
+
+/*
+ * One iteration of continual KV cache compression (Algorithm 1; Sec. 3):
+ * append the new rows (ipv_append), and if the cache then holds
+ * len >= mem_cap rows, compress it to `budget` rows (ipv_compress with the
+ * given alpha, recent_frames and cv_tau). *n_out (host) receives the row
+ * count after the step and *compressed (host) whether the pass ran.
+ * Needs budget <= mem_cap <= S and n_tokens < mem_cap (the previous step
+ * left the cache below the cap). Positions: the cache holds keys before the
+ * rotary position encoding and compaction keeps the order of the kept rows,
+ * so after every step row j takes position j at decoding, which stays below
+ * mem_cap + rows (appendix, positional-encoding details); no position array
+ * is stored.
+ */
+ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                        int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                        int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
+                        const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
+                        int32_t* n_out, int32_t* compressed, void* stream);
 
 /* Reset the workspace's device error word (a small kernel on `stream`). */
 ipv_status ipv_clear_device_errors(void* ws, size_t ws_bytes, void* stream);

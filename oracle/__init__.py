@@ -179,3 +179,29 @@ def compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames
                                _ptr(_c(patch_idx, np.int32)), n, budget, tar_budget_total(alpha, budget),
                                recent_frames, _ptr(tau), _ptr(tar), _ptr(van), _ptr(keep), None), "compress")
     return tar, van, keep
+
+
+def append(K, V, frame_idx, patch_idx, n, K_new, V_new, frame_id, first_patch=0) -> int:
+    """Algorithm 1 step (1), in place: rows [n, n + rows) of every slice take
+    the new rows, frame id `frame_id` and patch ids first_patch, first_patch+1,
+    ...; returns the new row count."""
+    rows = K_new.shape[3]
+    if K_new.shape != V_new.shape or K_new.shape[:3] != K.shape[:3] or n + rows > K.shape[3]:
+        raise OracleError("append: rows do not fit")
+    K[:, :, :, n:n + rows] = K_new
+    V[:, :, :, n:n + rows] = V_new
+    frame_idx[:, :, :, n:n + rows] = frame_id
+    patch_idx[:, :, :, n:n + rows] = first_patch + np.arange(rows, dtype=np.int32)
+    return n + rows
+
+
+def ckv_step(K, V, frame_idx, patch_idx, n, K_new, V_new, frame_id, first_patch, mem_cap, budget, alpha,
+             recent_frames, grid_h, grid_w, cv_tau=None):
+    """One iteration of Algorithm 1, in place: append; if the cache then holds
+    len >= mem_cap rows, run the pass to `budget` rows. Returns
+    (new n, (tar32, van32, keep_idx) of the pass or None)."""
+    n = append(K, V, frame_idx, patch_idx, n, K_new, V_new, frame_id, first_patch)
+    if n < mem_cap:
+        return n, None
+    out = compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames, grid_h, grid_w, cv_tau)
+    return budget, out

@@ -240,6 +240,30 @@ ipv_status compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, in
   return IPV_ERR_SHAPE;
 }
 
+// ------------------------------------------------------------ append
+// Grid-stride copy of the new rows (16 bytes per thread and step) into rows
+// [n, n + rows) of every slice, then the metadata of those rows.
+__global__ __launch_bounds__(256) void k_append(const char* __restrict__ Kn, const char* __restrict__ Vn,
+                                                char* __restrict__ K, char* __restrict__ V,
+                                                int32_t* __restrict__ fr, int32_t* __restrict__ pa, int64_t S,
+                                                int32_t n, int32_t rows, int64_t RB, int32_t frame_id,
+                                                int32_t first_patch, int64_t slices) {
+  const int64_t per_row = RB / 16, per_slice = (int64_t)rows * per_row, total = slices * per_slice;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const int64_t slice = i / per_slice, rem = i % per_slice;
+    const int64_t dst = (slice * S + n) * RB + rem * 16;
+    const int64_t src = slice * rows * RB + rem * 16;
+    store16(K + dst, load16(Kn + src));
+    store16(V + dst, load16(Vn + src));
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < slices * rows; i += stride) {
+    const int64_t slice = i / rows, j = i % rows;
+    fr[slice * S + n + j] = frame_id;
+    pa[slice * S + n + j] = first_patch + (int32_t)j;
+  }
+}
+
 int32_t floor_share(double alpha, int32_t budget) { return (int32_t)std::floor(alpha * (double)budget); }
 
 ipv_status check_tau(const double* tau) {
@@ -368,6 +392,59 @@ ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame
                         float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream) {
   return ipv_compress_timed(shape, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar,
                             van, keep_idx, ws, ws_bytes, stream, nullptr);
+}
+
+ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                      int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                      int32_t first_patch, void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!K || !V || !frame_idx || !patch_idx || !K_new || !V_new) return IPV_ERR_NULL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
+      !aligned(K_new, 16) || !aligned(V_new, 16))
+    return IPV_ERR_ALIGN;
+  if (n_tokens < 0 || rows < 1 || (int64_t)n_tokens + rows > d.S) return IPV_ERR_SHAPE;
+  if (first_patch < 0 || (int64_t)first_patch + rows > d.p) return IPV_ERR_ARG;
+  const int64_t RB = d.D * d.elem;
+  const int64_t chunks = d.slices * rows * (RB / 16);
+  const uint32_t blocks = (uint32_t)std::min<int64_t>((chunks + 255) / 256, 65536);
+  k_append<<<dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream)>>>(
+      static_cast<const char*>(K_new), static_cast<const char*>(V_new), static_cast<char*>(K), static_cast<char*>(V),
+      frame_idx, patch_idx, d.S, n_tokens, rows, RB, frame_id, first_patch, d.slices);
+  return launched();
+}
+
+ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                        int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                        int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
+                        const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
+                        int32_t* n_out, int32_t* compressed, void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!n_out || !compressed) return IPV_ERR_NULL;
+  if (mem_cap < 1 || mem_cap > d.S || n_tokens >= mem_cap) return IPV_ERR_SHAPE;
+  if (budget > mem_cap) return IPV_ERR_BUDGET;
+  const int32_t n1 = n_tokens + rows;
+  if (n1 >= mem_cap) {
+    // every argument of the pass is checked before the append is enqueued
+    if (!tar || !van || !keep_idx) return IPV_ERR_NULL;
+    if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
+    IPV_TRY(check_rows(d, n1));
+    IPV_TRY(check_recent(d, recent_frames));
+    if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
+    IPV_TRY(check_budget(d, n1, budget, recent_frames));
+    IPV_TRY(check_tau(cv_tau));
+    IPV_TRY(check_ws(d, ws, ws_bytes));
+  }
+  IPV_TRY(ipv_append(shape, K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, rows, frame_id, first_patch, stream));
+  *n_out = n1;
+  *compressed = 0;
+  if (n1 < mem_cap) return IPV_OK;
+  IPV_TRY(ipv_compress(shape, K, V, frame_idx, patch_idx, n1, budget, alpha, recent_frames, cv_tau, tar, van,
+                       keep_idx, ws, ws_bytes, stream));
+  *n_out = budget;
+  *compressed = 1;
+  return IPV_OK;
 }
 
 ipv_status ipv_clear_device_errors(void* ws, size_t ws_bytes, void* stream) {

@@ -29,8 +29,8 @@ BF16, F32 = 0, 1
 DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN, DEV_WAIT_TIMEOUT = 1, 2, 4, 8, 16, 32
 
 EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
-           "ipv_compress", "ipv_compress_timed", "ipv_clear_device_errors", "ipv_read_device_errors",
-           "ipv_status_str")
+           "ipv_compress", "ipv_compress_timed", "ipv_append", "ipv_ckv_step", "ipv_clear_device_errors",
+           "ipv_read_device_errors", "ipv_status_str")
 
 
 class IpvError(RuntimeError):
@@ -74,6 +74,9 @@ def lib() -> ctypes.CDLL:
         L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, vp, vp, vp, vp, vp, sz, vp]
         L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, vp, vp, vp, vp, vp, sz, vp,
                                          ctypes.POINTER(Events)]
+        L.ipv_append.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, vp]
+        L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f64, i32, vp, vp, vp,
+                                   vp, vp, sz, ctypes.POINTER(i32), ctypes.POINTER(i32), vp]
         L.ipv_clear_device_errors.argtypes = [vp, sz, vp]
         L.ipv_read_device_errors.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
         L.ipv_status_str.argtypes = [ctypes.c_int]
@@ -186,6 +189,38 @@ def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, rece
                                     None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
                                     _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(events)),
            "ipv_compress_timed")
+
+
+def ipv_append(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, first_patch, grid_h, grid_w,
+               stream=None) -> int:
+    """Append K_new/V_new ([B, L, H, rows, D]) after row n_tokens of every
+    slice; returns the new row count."""
+    s = shape_of(K, grid_h, grid_w)
+    if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
+            or K_new.shape[4] != K.shape[4] or K_new.dtype != K.dtype:
+        raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
+    rows = K_new.shape[3]
+    _check(lib().ipv_append(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                            _ptr(K_new), _ptr(V_new), rows, frame_id, first_patch, _stream(stream)), "ipv_append")
+    return n_tokens + rows
+
+
+def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, first_patch, mem_cap, budget,
+                 alpha, recent_frames, cv_tau, tar, van, keep_idx, ws, grid_h, grid_w, stream=None):
+    """Append, then compress to `budget` once the cache holds >= mem_cap rows.
+    Returns (new row count, whether the pass ran)."""
+    s = shape_of(K, grid_h, grid_w)
+    if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
+            or K_new.shape[4] != K.shape[4] or K_new.dtype != K.dtype:
+        raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
+    tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
+    n_out, comp = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().ipv_ckv_step(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+                              _ptr(K_new), _ptr(V_new), K_new.shape[3], frame_id, first_patch, mem_cap, budget,
+                              float(alpha), recent_frames, None if tau is None else ctypes.addressof(tau), _ptr(tar),
+                              _ptr(van), _ptr(keep_idx), _ptr(ws), 0 if ws is None else ws.numel(),
+                              ctypes.byref(n_out), ctypes.byref(comp), _stream(stream)), "ipv_ckv_step")
+    return n_out.value, bool(comp.value)
 
 
 def ipv_clear_device_errors(ws, stream=None):

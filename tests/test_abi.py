@@ -139,3 +139,28 @@ def test_binding_fails_loudly_without_the_library(monkeypatch):
     monkeypatch.setattr(ipv, "LIB_PATH", "/nonexistent/libipv.so")
     with pytest.raises(ipv.IpvError):
         ipv.lib()
+
+
+def test_append_and_ckv_step_validate_before_launch():
+    L, s = ipv.lib(), shape()
+    big = 1 << 40
+    # ipv_append(shape, K, V, fr, pa, n, K_new, V_new, rows, frame_id, first_patch, stream)
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, None, FAKE, 196, 0, 0, None) == ipv.ERR_NULL
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE + 4, FAKE, 196, 0, 0, None) == ipv.ERR_ALIGN
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6200, FAKE, FAKE, 196, 0, 0, None) == ipv.ERR_SHAPE
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, 0, 0, 0, None) == ipv.ERR_SHAPE
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, 100, 0, 97, None) == ipv.ERR_ARG
+    n_out, comp = ctypes.c_int32(), ctypes.c_int32()
+
+    def step(n=6076, rows=196, cap=6272, budget=3136, tar=FAKE, ws=FAKE, wsb=big, nout=True):
+        return L.ipv_ckv_step(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, n, FAKE, FAKE, rows, 30, 0, cap, budget, 0.5,
+                              4, None, tar, FAKE, FAKE, ws, wsb, ctypes.byref(n_out) if nout else None,
+                              ctypes.byref(comp), None)
+
+    assert step(nout=False) == ipv.ERR_NULL
+    assert step(n=6272) == ipv.ERR_SHAPE          # the previous step left the cache at the cap
+    assert step(cap=7000) == ipv.ERR_SHAPE        # cap beyond the capacity
+    assert step(budget=6300) == ipv.ERR_BUDGET    # budget above the cap
+    assert step(tar=None) == ipv.ERR_NULL         # the pass would run: its arguments are checked first
+    assert step(wsb=0) == ipv.ERR_WORKSPACE
+    assert step(budget=700) == ipv.ERR_BUDGET     # smaller than the recent window
