@@ -25,6 +25,8 @@ _SRC = os.path.join(_HERE, "ipv_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 OK, ERR_ARG, ERR_META, ERR_BUDGET, ERR_NAN = 0, -1, -2, -3, -4
+# variant bits (the ablation rows of Tab. 5 and the head-shared reading)
+TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED = 1, 2, 4, 8
 
 
 class OracleError(RuntimeError):
@@ -62,11 +64,12 @@ def lib():
         L = ctypes.CDLL(_LIB)
         vp, i32 = ctypes.c_void_p, ctypes.c_int32
         sp = ctypes.POINTER(Shape)
-        L.ipvo_tar_scores.argtypes = [sp, vp, vp, vp, i32, i32, vp]
+        u32 = ctypes.c_uint32
+        L.ipvo_tar_scores.argtypes = [sp, vp, vp, vp, i32, i32, u32, vp]
         L.ipvo_van_scores.argtypes = [sp, vp, vp, vp, i32, vp, vp, vp]
-        L.ipvo_select.argtypes = [sp, vp, vp, vp, i32, i32, i32, i32, vp, vp]
+        L.ipvo_select.argtypes = [sp, vp, vp, vp, i32, i32, i32, i32, u32, vp, vp]
         L.ipvo_compact.argtypes = [sp, vp, vp, vp, vp, i32, vp, i32]
-        L.ipvo_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp]
+        L.ipvo_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, i32, i32, u32, vp, vp, vp, vp, vp]
         for f in (L.ipvo_tar_scores, L.ipvo_van_scores, L.ipvo_select, L.ipvo_compact, L.ipvo_compress):
             f.restype = ctypes.c_int
         L.ipvo_max_threads.restype = ctypes.c_int32
@@ -111,12 +114,13 @@ def _check(rc: int, what: str):
         raise OracleError("%s failed with code %d" % (what, rc))
 
 
-def tar_scores(K, frame_idx, patch_idx, n, recent_frames, grid_h, grid_w) -> np.ndarray:
-    """TaR scores in fp64, [B, L, H, S] (rows >= n left at 0)."""
+def tar_scores(K, frame_idx, patch_idx, n, recent_frames, grid_h, grid_w, mode=0) -> np.ndarray:
+    """TaR scores in fp64, [B, L, H, S] (rows >= n left at 0). mode & TAR_ADJACENT:
+    against the previous frame's key at the same position instead of the recent window."""
     s = _shape(K, grid_h, grid_w)
     out = np.zeros(K.shape[:4], np.float64)
     _check(lib().ipvo_tar_scores(ctypes.byref(s), _ptr(K), _ptr(_c(frame_idx, np.int32)),
-                                 _ptr(_c(patch_idx, np.int32)), n, recent_frames, _ptr(out)), "tar_scores")
+                                 _ptr(_c(patch_idx, np.int32)), n, recent_frames, mode, _ptr(out)), "tar_scores")
     return out
 
 
@@ -142,8 +146,10 @@ class Selection:
     cut_van: np.ndarray
 
 
-def select(tar32, van32, frame_idx, n, budget, alpha, recent_frames, grid_h=1, grid_w=1) -> Selection:
-    """Keep set from fp32 scores (the precision the decision is taken in)."""
+def select(tar32, van32, frame_idx, n, budget, alpha, recent_frames, grid_h=1, grid_w=1, mode=0) -> Selection:
+    """Keep set from fp32 scores (the precision the decision is taken in). mode:
+    TAR_REVERSE / VAN_REVERSE take a stage's lowest scores; HEAD_SHARED ranks
+    the fp32 sum over each layer's heads and gives every head the same rows."""
     tar32 = _c(tar32, np.float32)
     van32 = _c(van32, np.float32)
     B, L, H, S = tar32.shape
@@ -151,7 +157,7 @@ def select(tar32, van32, frame_idx, n, budget, alpha, recent_frames, grid_h=1, g
     keep = np.zeros((B, L, H, budget), np.int32)
     info = (SelectInfo * (B * L * H))()
     _check(lib().ipvo_select(ctypes.byref(s), _ptr(tar32), _ptr(van32), _ptr(_c(frame_idx, np.int32)), n,
-                             budget, tar_budget_total(alpha, budget), recent_frames, _ptr(keep),
+                             budget, tar_budget_total(alpha, budget), recent_frames, mode, _ptr(keep),
                              ctypes.addressof(info)), "select")
     f = lambda name, dt: np.array([getattr(i, name) for i in info], dt).reshape(B, L, H)
     return Selection(keep, f("n_recent", np.int32), f("b_tar", np.int32), f("b_van", np.int32),
@@ -168,7 +174,8 @@ def compact(K, V, frame_idx, patch_idx, n, keep_idx, grid_h=1, grid_w=1):
     return K, V, fr, pa
 
 
-def compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames, grid_h, grid_w, cv_tau=None):
+def compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames, grid_h, grid_w, cv_tau=None,
+                     mode=0):
     """The whole pass, in place on the given arrays; returns (tar32, van32, keep_idx)."""
     s = _shape(K, grid_h, grid_w)
     tar = np.zeros(K.shape[:4], np.float32)
@@ -177,7 +184,8 @@ def compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames
     tau = None if cv_tau is None else np.asarray(cv_tau, np.float64)
     _check(lib().ipvo_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(_c(frame_idx, np.int32)),
                                _ptr(_c(patch_idx, np.int32)), n, budget, tar_budget_total(alpha, budget),
-                               recent_frames, _ptr(tau), _ptr(tar), _ptr(van), _ptr(keep), None), "compress")
+                               recent_frames, mode, _ptr(tau), _ptr(tar), _ptr(van), _ptr(keep), None),
+           "compress")
     return tar, van, keep
 
 
@@ -196,12 +204,13 @@ def append(K, V, frame_idx, patch_idx, n, K_new, V_new, frame_id, first_patch=0)
 
 
 def ckv_step(K, V, frame_idx, patch_idx, n, K_new, V_new, frame_id, first_patch, mem_cap, budget, alpha,
-             recent_frames, grid_h, grid_w, cv_tau=None):
+             recent_frames, grid_h, grid_w, cv_tau=None, mode=0):
     """One iteration of Algorithm 1, in place: append; if the cache then holds
     len >= mem_cap rows, run the pass to `budget` rows. Returns
     (new n, (tar32, van32, keep_idx) of the pass or None)."""
     n = append(K, V, frame_idx, patch_idx, n, K_new, V_new, frame_id, first_patch)
     if n < mem_cap:
         return n, None
-    out = compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames, grid_h, grid_w, cv_tau)
+    out = compress_inplace(K, V, frame_idx, patch_idx, n, budget, alpha, recent_frames, grid_h, grid_w, cv_tau,
+                           mode)
     return budget, out

@@ -23,6 +23,20 @@
  *                       recent window is always kept
  *   compaction          Sec. 3.1 / Algorithm 1 step (5): K <- K[I], V <- V[I]
  *
+ * Variants (Tab. 5 ablation rows and the head-shared reading of the scores),
+ * chosen by the `mode` bits:
+ *   IPVO_TAR_REVERSE    the TaR stage keeps the lowest TaR scores (TaR Reverse)
+ *   IPVO_VAN_REVERSE    the VaN stage keeps the lowest VaN scores (VaN Reverse)
+ *   IPVO_TAR_ADJACENT   a past key is compared with the key at its patch
+ *                       position in the closest earlier frame that still has
+ *                       one (consecutive-frame similarity, Sec. 3.1 and its
+ *                       figure on static patches between adjacent frames),
+ *                       instead of with the r recent frames
+ *   IPVO_HEAD_SHARED    one keep set per (stream, layer): each stage ranks the
+ *                       fp32 sum over the layer's heads of their scores (the
+ *                       head-free s(t, i, j) and K[:, I, :] of Sec. 3.1-3.3),
+ *                       and every head keeps the same rows
+ *
  * Readings where the paper is silent (documented with the design notes):
  *   - cos(a, b) = 0 when |a||b| = 0; a patch with no key in the recent window
  *     scores 0; -0.0 is written as +0.0.
@@ -56,6 +70,7 @@ typedef struct {
 } ipvo_select_info;
 
 enum { IPVO_OK = 0, IPVO_ERR_ARG = -1, IPVO_ERR_META = -2, IPVO_ERR_BUDGET = -3, IPVO_ERR_NAN = -4 };
+enum { IPVO_TAR_REVERSE = 1, IPVO_VAN_REVERSE = 2, IPVO_TAR_ADJACENT = 4, IPVO_HEAD_SHARED = 8, IPVO_MODES = 15 };
 
 static int shape_ok(const ipvo_shape* s, int32_t n) {
   if (!s) return 0;
@@ -115,10 +130,14 @@ static double cosine(const ipvo_shape* s, const void* K, int64_t sl, int64_t a, 
  * for a past row x at patch position q, minus the mean of cos(K[x], K[y]) over
  * the recent rows y at the same position q. Recent rows get 0 (they are kept
  * regardless). Rows [n, S) are not written.
+ * IPVO_TAR_ADJACENT: minus cos(K[x], K[y]) for the one row y at position q
+ * whose frame is the latest frame before x's that has a row at q (0 if no
+ * earlier frame has one).
  */
 int ipvo_tar_scores(const ipvo_shape* s, const void* K, const int32_t* frame_idx, const int32_t* patch_idx,
-                    int32_t n, int32_t recent_frames, double* tar) {
+                    int32_t n, int32_t recent_frames, uint32_t mode, double* tar) {
   if (!shape_ok(s, n) || !K || !frame_idx || !patch_idx || !tar || recent_frames < 1) return IPVO_ERR_ARG;
+  if (mode & ~(uint32_t)IPVO_MODES) return IPVO_ERR_ARG;
   const int32_t p = s->grid_h * s->grid_w;
   int err = 0;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
@@ -134,10 +153,21 @@ int ipvo_tar_scores(const ipvo_shape* s, const void* K, const int32_t* frame_idx
       if (rec[x]) { out[x] = 0.0; continue; }
       double sum = 0.0;
       int32_t count = 0;
-      for (int32_t y = n - nr; y < n; ++y) {
-        if (pa[y] != pa[x]) continue;
-        sum += cosine(s, K, sl, x, y);
-        count += 1;
+      if (mode & IPVO_TAR_ADJACENT) {
+        /* frame ids do not decrease along the rows: walk back to the first
+           row at position q that lies in an earlier frame */
+        for (int32_t y = x - 1; y >= 0; --y)
+          if (pa[y] == pa[x] && fr[y] < fr[x]) {
+            sum = cosine(s, K, sl, x, y);
+            count = 1;
+            break;
+          }
+      } else {
+        for (int32_t y = n - nr; y < n; ++y) {
+          if (pa[y] != pa[x]) continue;
+          sum += cosine(s, K, sl, x, y);
+          count += 1;
+        }
       }
       double v = count ? -(sum / count) : 0.0;
       out[x] = (v == 0.0) ? 0.0 : v; /* -0.0 -> +0.0 */
@@ -258,6 +288,68 @@ static int by_score_desc(const void* pa, const void* pb, void* ctx) {
   return (a > b) - (a < b);
 }
 
+/* Reverse order (the ablation's reversed stages): lower score first, equal
+   scores by lower row index. */
+static int by_score_asc(const void* pa, const void* pb, void* ctx) {
+  const float* sc = (const float*)ctx;
+  int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
+  if (sc[a] < sc[b]) return -1;
+  if (sc[a] > sc[b]) return 1;
+  return (a > b) - (a < b);
+}
+
+/*
+ * One keep set from one pair of fp32 score columns and one frame column.
+ * Returns an error bit (0 on success) and fills keep_idx[0..budget) and *inf.
+ */
+static int select_one(const float* st, const float* sv, const int32_t* fr, int32_t n, int32_t budget,
+                      int32_t tar_budget_total, int32_t recent_frames, uint32_t mode, int32_t* keep_idx,
+                      ipvo_select_info* info) {
+  unsigned char* rec = malloc((size_t)n);
+  unsigned char* keep = calloc((size_t)n, 1);
+  int32_t* order = malloc(sizeof(int32_t) * (size_t)n);
+  int err = 0;
+  int32_t nr = recent_window(fr, n, recent_frames, rec);
+  ipvo_select_info inf = {nr, 0, 0, 0, NAN, NAN};
+  if (nr < 0) err |= 2;
+  else if (nr > budget) err |= 4;
+  else {
+    for (int32_t x = 0; x < n; ++x)
+      if (!rec[x] && (isnan(st[x]) || isnan(sv[x]))) err |= 8;
+    int32_t bt = tar_budget_total - nr;
+    if (bt < 0) bt = 0;
+    int32_t bv = budget - nr - bt;
+    inf.b_tar = bt;
+    inf.b_van = bv;
+    for (int32_t x = 0; x < n; ++x) keep[x] = rec[x];
+    /* TaR stage over the past rows */
+    int32_t m = 0;
+    for (int32_t x = 0; x < n; ++x)
+      if (!rec[x]) order[m++] = x;
+    qsort_r(order, (size_t)m, sizeof(int32_t), (mode & IPVO_TAR_REVERSE) ? by_score_asc : by_score_desc,
+            (void*)st);
+    for (int32_t i = 0; i < bt; ++i) keep[order[i]] = 1;
+    if (bt > 0) inf.cut_tar = st[order[bt - 1]];
+    /* VaN stage over the past rows TaR did not pick */
+    m = 0;
+    for (int32_t x = 0; x < n; ++x)
+      if (!keep[x]) order[m++] = x;
+    qsort_r(order, (size_t)m, sizeof(int32_t), (mode & IPVO_VAN_REVERSE) ? by_score_asc : by_score_desc,
+            (void*)sv);
+    for (int32_t i = 0; i < bv; ++i) keep[order[i]] = 1;
+    if (bv > 0) inf.cut_van = sv[order[bv - 1]];
+    int32_t j = 0;
+    for (int32_t x = 0; x < n; ++x)
+      if (keep[x]) keep_idx[j++] = x;
+    if (j != budget) err |= 16;
+  }
+  *info = inf;
+  free(rec);
+  free(keep);
+  free(order);
+  return err;
+}
+
 /*
  * Keep-set selection (Algorithm 1 steps (3)-(5); Sec. 3.3). Scores are fp32,
  * the precision the GPU decides in. With R the recent window:
@@ -266,57 +358,49 @@ static int by_score_desc(const void* pa, const void* pb, void* ctx) {
  *   V = the b_V past rows outside T with the highest VaN score
  *   keep = R u T u V, ascending.
  * tar_budget_total = floor(alpha * C) computed by the caller in double.
+ * IPVO_TAR_REVERSE / IPVO_VAN_REVERSE: that stage takes the lowest scores.
+ * IPVO_HEAD_SHARED: per (stream, layer), the scores of heads 0..H-1 are added
+ * in that order in fp32, every head must hold the same frame ids, and the one
+ * keep set (and info) is written for every head.
  */
 int ipvo_select(const ipvo_shape* s, const float* tar, const float* van, const int32_t* frame_idx, int32_t n,
-                int32_t budget, int32_t tar_budget_total, int32_t recent_frames, int32_t* keep_idx,
+                int32_t budget, int32_t tar_budget_total, int32_t recent_frames, uint32_t mode, int32_t* keep_idx,
                 ipvo_select_info* info) {
   if (!shape_ok(s, n) || !tar || !van || !frame_idx || !keep_idx || recent_frames < 1) return IPVO_ERR_ARG;
+  if (mode & ~(uint32_t)IPVO_MODES) return IPVO_ERR_ARG;
   if (budget < 1 || budget > n || tar_budget_total < 0 || tar_budget_total > budget) return IPVO_ERR_BUDGET;
+  const int64_t S = s->capacity;
+  const int32_t G = (mode & IPVO_HEAD_SHARED) ? s->kv_heads : 1; /* slices that share one keep set */
   int err = 0;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
-  for (int64_t sl = 0; sl < n_slices(s); ++sl) {
-    const int64_t S = s->capacity;
-    const float* st = tar + sl * S;
-    const float* sv = van + sl * S;
-    unsigned char* rec = malloc((size_t)n);
-    unsigned char* keep = calloc((size_t)n, 1);
-    int32_t* order = malloc(sizeof(int32_t) * (size_t)n);
-    int32_t nr = recent_window(frame_idx + sl * S, n, recent_frames, rec);
-    ipvo_select_info inf = {nr, 0, 0, 0, NAN, NAN};
-    if (nr < 0) err |= 2;
-    else if (nr > budget) err |= 4;
-    else {
-      for (int32_t x = 0; x < n; ++x)
-        if (!rec[x] && (isnan(st[x]) || isnan(sv[x]))) err |= 8;
-      int32_t bt = tar_budget_total - nr;
-      if (bt < 0) bt = 0;
-      int32_t bv = budget - nr - bt;
-      inf.b_tar = bt;
-      inf.b_van = bv;
-      for (int32_t x = 0; x < n; ++x) keep[x] = rec[x];
-      /* TaR stage over the past rows */
-      int32_t m = 0;
-      for (int32_t x = 0; x < n; ++x)
-        if (!rec[x]) order[m++] = x;
-      qsort_r(order, (size_t)m, sizeof(int32_t), by_score_desc, (void*)st);
-      for (int32_t i = 0; i < bt; ++i) keep[order[i]] = 1;
-      if (bt > 0) inf.cut_tar = st[order[bt - 1]];
-      /* VaN stage over the past rows TaR did not pick */
-      m = 0;
-      for (int32_t x = 0; x < n; ++x)
-        if (!keep[x]) order[m++] = x;
-      qsort_r(order, (size_t)m, sizeof(int32_t), by_score_desc, (void*)sv);
-      for (int32_t i = 0; i < bv; ++i) keep[order[i]] = 1;
-      if (bv > 0) inf.cut_van = sv[order[bv - 1]];
-      int32_t j = 0;
-      for (int32_t x = 0; x < n; ++x)
-        if (keep[x]) keep_idx[sl * budget + (j++)] = x;
-      if (j != budget) err |= 16;
+  for (int64_t grp = 0; grp < n_slices(s) / G; ++grp) {
+    const int64_t sl0 = grp * G;
+    ipvo_select_info inf;
+    if (G == 1) {
+      err |= select_one(tar + sl0 * S, van + sl0 * S, frame_idx + sl0 * S, n, budget, tar_budget_total,
+                        recent_frames, mode, keep_idx + sl0 * budget, &inf);
+    } else {
+      float* st = malloc(sizeof(float) * (size_t)n);
+      float* sv = malloc(sizeof(float) * (size_t)n);
+      for (int32_t x = 0; x < n; ++x) {
+        float a = 0.0f, b = 0.0f;
+        for (int32_t h = 0; h < G; ++h) {
+          a += tar[(sl0 + h) * S + x];
+          b += van[(sl0 + h) * S + x];
+          if (frame_idx[(sl0 + h) * S + x] != frame_idx[sl0 * S + x]) err |= 2;
+        }
+        st[x] = a;
+        sv[x] = b;
+      }
+      err |= select_one(st, sv, frame_idx + sl0 * S, n, budget, tar_budget_total, recent_frames, mode,
+                        keep_idx + sl0 * budget, &inf);
+      for (int32_t h = 1; h < G; ++h)
+        memcpy(keep_idx + (sl0 + h) * budget, keep_idx + sl0 * budget, sizeof(int32_t) * (size_t)budget);
+      free(st);
+      free(sv);
     }
-    if (info) info[sl] = inf;
-    free(rec);
-    free(keep);
-    free(order);
+    if (info)
+      for (int32_t h = 0; h < G; ++h) info[sl0 + h] = inf;
   }
   if (err & 2) return IPVO_ERR_META;
   if (err & 4) return IPVO_ERR_BUDGET;
@@ -376,8 +460,8 @@ int ipvo_compact(const ipvo_shape* s, void* K, void* V, int32_t* frame_idx, int3
  * place. tar/van/keep_idx/info may be NULL (scratch is allocated here).
  */
 int ipvo_compress(const ipvo_shape* s, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx, int32_t n,
-                  int32_t budget, int32_t tar_budget_total, int32_t recent_frames, const double* cv_tau,
-                  float* tar_out, float* van_out, int32_t* keep_out, ipvo_select_info* info) {
+                  int32_t budget, int32_t tar_budget_total, int32_t recent_frames, uint32_t mode,
+                  const double* cv_tau, float* tar_out, float* van_out, int32_t* keep_out, ipvo_select_info* info) {
   if (!shape_ok(s, n)) return IPVO_ERR_ARG;
   const int64_t cells = n_slices(s) * s->capacity;
   double* tar = calloc((size_t)cells, sizeof(double));
@@ -385,7 +469,7 @@ int ipvo_compress(const ipvo_shape* s, void* K, void* V, int32_t* frame_idx, int
   float* tf = tar_out ? tar_out : calloc((size_t)cells, sizeof(float));
   float* vf = van_out ? van_out : calloc((size_t)cells, sizeof(float));
   int32_t* keep = keep_out ? keep_out : malloc(sizeof(int32_t) * (size_t)(n_slices(s) * budget));
-  int rc = ipvo_tar_scores(s, K, frame_idx, patch_idx, n, recent_frames, tar);
+  int rc = ipvo_tar_scores(s, K, frame_idx, patch_idx, n, recent_frames, mode, tar);
   if (rc == IPVO_OK) rc = ipvo_van_scores(s, V, frame_idx, patch_idx, n, cv_tau, van, NULL);
   if (rc == IPVO_OK) {
     for (int64_t sl = 0; sl < n_slices(s); ++sl)
@@ -393,7 +477,7 @@ int ipvo_compress(const ipvo_shape* s, void* K, void* V, int32_t* frame_idx, int
         tf[sl * s->capacity + x] = (float)tar[sl * s->capacity + x];
         vf[sl * s->capacity + x] = (float)van[sl * s->capacity + x];
       }
-    rc = ipvo_select(s, tf, vf, frame_idx, n, budget, tar_budget_total, recent_frames, keep, info);
+    rc = ipvo_select(s, tf, vf, frame_idx, n, budget, tar_budget_total, recent_frames, mode, keep, info);
   }
   if (rc == IPVO_OK) rc = ipvo_compact(s, K, V, frame_idx, patch_idx, n, keep, budget);
   free(tar);
