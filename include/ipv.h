@@ -18,6 +18,10 @@
  *   ipv_append       add a frame's rows to the cache (Algorithm 1 step (1))
  *   ipv_ckv_step     append, then compress when the memory cap is reached
  *
+ * A `mode` argument (IPV_MODE_* bits, 0 = the method as published) selects the
+ * variants of the paper's ablation (Tab. 5: TaR Reverse, VaN Reverse, TaR
+ * between consecutive frames) and the head-shared reading of the scores.
+ *
  * ---------------------------------------------------------------- layouts
  * A cache holds B streams x L layers x H KV heads; each (b, l, h) "slice" has
  * a row capacity S of which rows [0, n) are valid (n = n_tokens, the same for
@@ -85,12 +89,35 @@ typedef enum { IPV_BF16 = 0, IPV_F32 = 1 } ipv_dtype;
 /* Device error word bits (accumulated with atomic OR until cleared). */
 enum {
   IPV_DEV_BAD_PATCH = 1u,      /* patch_idx outside [0, p): the row scored 0 / was left out of pooling */
-  IPV_DEV_BAD_FRAMES = 2u,     /* frame ids decrease, or a (frame, patch) pair repeats in the window */
+  IPV_DEV_BAD_FRAMES = 2u,     /* frame ids decrease, a (frame, patch) pair repeats in the window (in any
+                                  row with IPV_TAR_ADJACENT), or heads differ with IPV_HEAD_SHARED */
   IPV_DEV_RECENT_OVER = 4u,    /* recent window larger than the budget: keep_idx set to 0..C-1 */
   IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n): row j was not moved */
   IPV_DEV_NAN = 16u,           /* a candidate score is NaN: its rank is unspecified */
   IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired (e.g. a workspace shared by
                                   overlapping calls); its rows were not moved */
+};
+
+/*
+ * Variant bits of the `mode` argument. Calls ignore the bits that do not
+ * concern their step and reject unknown bits with IPV_ERR_ARG.
+ */
+enum {
+  /* the TaR stage keeps the b_T past rows with the LOWEST tar (Tab. 5, TaR Reverse) */
+  IPV_TAR_REVERSE = 1u,
+  /* the VaN stage keeps the b_V rows with the LOWEST van (Tab. 5, VaN Reverse; Sec. 3.2) */
+  IPV_VAN_REVERSE = 2u,
+  /* TaR between consecutive frames (Sec. 3.1 and its figure on static patches of
+     adjacent frames): a past row x at position q is compared with the one row
+     at q in the latest earlier frame that holds q:
+       tar[x] = -cos(K[x], K[y]),  0 if no earlier frame holds q. */
+  IPV_TAR_ADJACENT = 4u,
+  /* one keep set per (stream, layer) (the head-free s(t, i, j) and K[:, I, :] of
+     Sec. 3.1-3.3): each stage ranks, per row, the sum over the layer's heads of
+     their scores (fp32, heads added in order 0..H-1 starting from +0); every head
+     must hold the same frame ids and receives the same keep_idx row. */
+  IPV_HEAD_SHARED = 8u,
+  IPV_MODE_ALL = 15u
 };
 
 typedef struct {
@@ -113,10 +140,11 @@ ipv_status ipv_workspace_bytes(const ipv_shape* shape, size_t* bytes);
  * with cos = 0 when either key is zero, and tar[x] = 0 when r_q = 0 (a
  * position missing from a partial recent frame). Recent rows get 0. -0.0 is
  * written as +0.0. fp32 accumulation. Requires 1 <= r <= 256 and r * p <= 65536.
+ * mode & IPV_TAR_ADJACENT: the consecutive-frame score described at that bit.
  */
 ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* frame_idx,
-                          const int32_t* patch_idx, int32_t n_tokens, int32_t recent_frames, float* tar,
-                          void* ws, size_t ws_bytes, void* stream);
+                          const int32_t* patch_idx, int32_t n_tokens, int32_t recent_frames, uint32_t mode,
+                          float* tar, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * VaN score (Sec. 3.2): van[x] = ||V[x]||_2 for every valid row, fp32.
@@ -139,10 +167,12 @@ ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* 
  *   with the highest van; equal scores go to the lower row index, -0.0 == +0.0.
  *   keep_idx = R u T u V in ascending order.
  * Requires min(n, r*p) <= C <= n and n <= 65536.
+ * mode: IPV_TAR_REVERSE / IPV_VAN_REVERSE take a stage's lowest scores (ties
+ * still to the lower row index); IPV_HEAD_SHARED selects once per layer.
  */
 ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van, const int32_t* frame_idx,
-                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, int32_t* keep_idx,
-                      void* ws, size_t ws_bytes, void* stream);
+                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                      int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * In-place compaction (Sec. 3.1; Algorithm 1 step (5)): for j < C, row j of
@@ -156,9 +186,11 @@ ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_
                        int32_t n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
                        void* stream);
 
-/* The whole pass: ipv_tar_scores, ipv_van_scores, ipv_select, ipv_compact. */
+/* The whole pass: ipv_tar_scores, ipv_van_scores, ipv_select, ipv_compact,
+   each with the same mode (with IPV_TAR_ADJACENT the VaN scores are computed
+   in the same sweep as the consecutive-frame TaR scores). */
 ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
                         const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
                         size_t ws_bytes, void* stream);
 
@@ -166,6 +198,7 @@ ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame
  * ipv_compress with per-kernel timing: each non-NULL entry of `at` is a
  * hipEvent_t (created by the caller) recorded on `stream` at a step boundary:
  *   at[0] before the recent-key table   at[1] before the TaR/VaN sweep
+ *   (IPV_TAR_ADJACENT: before the prev-row walk, before the adjacent sweep)
  *   at[2] before pooling                at[3] before selection
  *   at[4] before compaction             at[5] after compaction
  * Elapsed time between consecutive events is that step's device time.
@@ -176,8 +209,8 @@ typedef struct {
 
 ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                               int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
-                              const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
-                              size_t ws_bytes, void* stream, const ipv_events* events);
+                              uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx,
+                              void* ws, size_t ws_bytes, void* stream, const ipv_events* events);
 
 /*
  * Append new rows to every slice (Algorithm 1 step (1): the tokens of a new
@@ -196,7 +229,7 @@ ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_i
  * One iteration of continual KV cache compression (Algorithm 1; Sec. 3):
  * append the new rows (ipv_append), and if the cache then holds
  * len >= mem_cap rows, compress it to `budget` rows (ipv_compress with the
- * given alpha, recent_frames and cv_tau). *n_out (host) receives the row
+ * given alpha, recent_frames, mode and cv_tau). *n_out (host) receives the row
  * count after the step and *compressed (host) whether the pass ran.
  * Needs budget <= mem_cap <= S and n_tokens < mem_cap (the previous step
  * left the cache below the cap). Positions: the cache holds keys before the
@@ -208,7 +241,7 @@ ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_i
 ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                         int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
                         int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
-                        const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
+                        uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
                         int32_t* n_out, int32_t* compressed, void* stream);
 
 /* Reset the workspace's device error word (a small kernel on `stream`). */

@@ -150,6 +150,10 @@ int ipvo_tar_scores(const ipvo_shape* s, const void* K, const int32_t* frame_idx
     if (nr < 0) { err |= 1; free(rec); continue; }
     for (int32_t x = 0; x < n; ++x) {
       if (pa[x] < 0 || pa[x] >= p) err |= 1;
+      /* consecutive-frame TaR needs each (frame, patch) pair at most once */
+      if (mode & IPVO_TAR_ADJACENT)
+        for (int32_t y = x - 1; y >= 0 && fr[y] == fr[x]; --y)
+          if (pa[y] == pa[x]) err |= 1;
       if (rec[x]) { out[x] = 0.0; continue; }
       double sum = 0.0;
       int32_t count = 0;

@@ -1,0 +1,205 @@
+// Consecutive-frame TaR: a past key is compared with one key only, the key at
+// its patch position in the closest earlier frame that still holds that
+// position (Sec. 3.1 measures static patches between adjacent frames; Tab. 5
+// contrasts TaR variants). Score -cos(K[x], K[prev(x)]), 0 with no such row.
+//
+// Two kernels:
+//   k_prev_rows       one 1024-thread block per slice walks the rows in chunks
+//                     of 1024 and writes prev(x) (or -1) for every valid row;
+//                     it also publishes the slice's first recent row and,
+//                     optionally, zeroes the slice's compaction flags.
+//   k_adjacent_sweep  the bandwidth part: for each past row, K[x] and
+//                     K[prev(x)] (and V[x] when VaN is fused), one dot product
+//                     and two norms per row.
+#pragma once
+
+#include "ipv_device.hpp"
+
+namespace ipv {
+
+constexpr int kPrevThreads = 1024;
+constexpr int kPrevMaxPositions = 8192;
+
+// prev(x), with frame ids non-decreasing along the rows: the latest row y < x
+// at x's patch position whose frame is older than x's. Inside a chunk a row
+// walks back over the chunk's own metadata (in LDS); if its position does not
+// occur earlier in the chunk, `last[q]` (the latest row at q in the chunks
+// before) is the answer. A second row with the same (frame, patch) pair, or a
+// frame id that decreases, or a patch id outside [0, p), sets an error bit;
+// such metadata gives no defined prev.
+//
+// The chunk metadata is double-buffered, so one chunk costs two barriers:
+// (A) the chunk's metadata is visible, (B) every walk has read `last` and the
+// carry; then `last` and the carry are updated for the next chunk.
+__global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __restrict__ frame_idx,
+                                                            const int32_t* __restrict__ patch_idx, int64_t S,
+                                                            int32_t n, int32_t r, int32_t p,
+                                                            int32_t* __restrict__ prev,
+                                                            int32_t* __restrict__ first_recent, uint32_t* err,
+                                                            uint32_t* __restrict__ zero, int32_t zero_per_slice) {
+  constexpr int NT = kPrevThreads;
+  __shared__ int32_t last[kPrevMaxPositions];
+  __shared__ int32_t cpa[2][NT], cfr[2][NT];
+  // carry: frame id of the previous chunk's last row, and the row its frame starts at
+  __shared__ int32_t carry_frame, carry_start;
+  const int tid = threadIdx.x;
+  const int64_t slice = blockIdx.x;
+  const int64_t base = slice * S;
+  if (zero)
+    for (int i = tid; i < zero_per_slice; i += NT) zero[slice * zero_per_slice + i] = 0u;
+  for (int q = tid; q < p; q += NT) last[q] = -1;
+  if (tid == 0) {
+    carry_frame = INT32_MIN;
+    carry_start = 0;
+  }
+  const int64_t thr = (int64_t)frame_idx[base + n - 1] - r + 1;
+  uint32_t ebits = 0;
+  int32_t nf = frame_idx[base + min((int64_t)tid, (int64_t)n - 1)];
+  int32_t np = patch_idx[base + min((int64_t)tid, (int64_t)n - 1)];
+  int b = 0;
+  for (int64_t c0 = 0; c0 < n; c0 += NT, b ^= 1) {
+    const int64_t x = c0 + tid;
+    const bool valid = x < n;
+    const int32_t f = nf, q = np;
+    cpa[b][tid] = q;
+    cfr[b][tid] = f;
+    __syncthreads();  // (A)
+    {  // the next chunk's metadata is on its way during the walks
+      const int64_t xn = min(c0 + NT + tid, (int64_t)n - 1);
+      nf = frame_idx[base + xn];
+      np = patch_idx[base + xn];
+    }
+    const int32_t cf = carry_frame, cs = carry_start;
+    const int cnt = (int)min((int64_t)NT, (int64_t)n - c0);
+    int32_t pred = -1;
+    if (valid) {
+      const int32_t fprev = tid > 0 ? cfr[b][tid - 1] : cf;
+      if (f < fprev) ebits |= 2u;
+      if ((int64_t)f >= thr && (int64_t)fprev < thr) first_recent[slice] = (int32_t)x;
+      if (q < 0 || q >= p) {
+        ebits |= 1u;
+      } else {
+        const int32_t* pa = cpa[b];
+        int y = tid - 1, hit = -1;
+        while (y >= 3) {
+          const int32_t a0 = pa[y], a1 = pa[y - 1], a2 = pa[y - 2], a3 = pa[y - 3];
+          if (a0 == q) { hit = y; break; }
+          if (a1 == q) { hit = y - 1; break; }
+          if (a2 == q) { hit = y - 2; break; }
+          if (a3 == q) { hit = y - 3; break; }
+          y -= 4;
+        }
+        if (hit < 0)
+          for (; y >= 0; --y)
+            if (pa[y] == q) {
+              hit = y;
+              break;
+            }
+        const bool past = (int64_t)f < thr;
+        if (hit >= 0) {
+          if (cfr[b][hit] < f) {
+            if (past) pred = (int32_t)(c0 + hit);
+          } else {
+            ebits |= 2u;  // the same (frame, patch) pair twice
+          }
+        } else {
+          const int32_t L = last[q];
+          if (L >= 0 && f == cf && L >= cs) ebits |= 2u;  // twice, across the chunk boundary
+          else if (past) pred = L;
+        }
+      }
+      prev[base + x] = pred;
+    }
+    __syncthreads();  // (B)
+    if (valid && q >= 0 && q < p) atomicMax(&last[q], (int32_t)x);
+    const int32_t fl = cfr[b][cnt - 1];
+    if (tid == cnt - 1) carry_frame = fl;
+    // the row where the last row's frame starts, if it starts in this chunk
+    if (valid && f == fl && (tid > 0 ? cfr[b][tid - 1] != fl : cf != fl)) carry_start = (int32_t)x;
+  }
+  if (ebits) raise_error(err, ebits);
+}
+
+// Rows are processed in natural order: a block covers GROUPS * U consecutive
+// rows, GROUPS rows (contiguous bytes) per step, one lane group of LPR lanes
+// (16 bytes each) per row. K[x] (past rows only) and V[x] loads go out with
+// the prev(x) loads; K[prev(x)] follows once prev(x) is known. Branch-free
+// buffer loads: a lane with nothing to read uses an offset past the end.
+template <typename T, int D, bool VAN>
+__global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K, const T* __restrict__ V,
+                                                        const int32_t* __restrict__ prev, int64_t S, int32_t n,
+                                                        const int32_t* __restrict__ first_recent,
+                                                        float* __restrict__ tar, float* __restrict__ van,
+                                                        int32_t blocks_per_slice, uint32_t n_work) {
+  constexpr int EPL = Lane<T>::EPL, LPR = D / EPL, GROUPS = 256 / LPR, U = 4;
+  constexpr uint32_t kSkip = 0xfffffff0u;
+  constexpr uint32_t RB = D * (uint32_t)sizeof(T);
+  const uint32_t logical = xcd_logical_id(blockIdx.x, gridDim.x);
+  if (logical >= n_work) return;
+  const int64_t slice = logical / blocks_per_slice;
+  const int64_t r0 = (int64_t)(logical % blocks_per_slice) * GROUPS * U;
+  const int tid = threadIdx.x, g = tid / LPR, lane = tid % LPR;
+  const int64_t base = slice * S;
+  const int32_t rec = first_recent[slice];
+  const uint32_t lo = (uint32_t)lane * EPL * (uint32_t)sizeof(T);
+  const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(K + base * D, (uint32_t)S * RB);
+  const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(V + base * D, (uint32_t)S * RB);
+  const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(prev + base, (uint32_t)(S * 4));
+  int32_t y[U];
+  Raw16 kx[U], ky[U], vx[U];
+  auto load = [](const __amdgpu_buffer_rsrc_t& rs, uint32_t off, Raw16& out) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    out.w[0] = v[0];
+    out.w[1] = v[1];
+    out.w[2] = v[2];
+    out.w[3] = v[3];
+  };
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t x = r0 + u * GROUPS + g;
+    const bool past = x < n && x < rec;
+    const int32_t yl = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, past ? (uint32_t)x * 4u : kSkip, 0, 0);
+    y[u] = past ? yl : -1;
+    load(krs, past ? (uint32_t)x * RB + lo : kSkip, kx[u]);
+    if (VAN) load(vrs, x < n ? (uint32_t)x * RB + lo : kSkip, vx[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) load(krs, y[u] >= 0 ? (uint32_t)y[u] * RB + lo : kSkip, ky[u]);
+  float tsc[U], vsc[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float a[EPL], c[EPL];
+    Lane<T>::decode(kx[u], a);
+    Lane<T>::decode(ky[u], c);
+    float dot = 0.f, aa = 0.f, cc = 0.f;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      dot += a[i] * c[i];
+      aa += a[i] * a[i];
+      cc += c[i] * c[i];
+    }
+    dot = group_sum<LPR>(dot);
+    aa = group_sum<LPR>(aa);
+    cc = group_sum<LPR>(cc);
+    float sc = (y[u] >= 0 && aa > 0.f && cc > 0.f) ? -(dot / (sqrtf(aa) * sqrtf(cc))) : 0.f;
+    if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
+    tsc[u] = sc;
+    if (VAN) {
+      float v[EPL];
+      Lane<T>::decode(vx[u], v);
+      float ss = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) ss += v[i] * v[i];
+      vsc[u] = sqrtf(group_sum<LPR>(ss));
+    }
+  }
+  if (lane < U) {
+    const int64_t x = r0 + lane * GROUPS + g;
+    if (x < n) {
+      tar[base + x] = lane == 0 ? tsc[0] : lane == 1 ? tsc[1] : lane == 2 ? tsc[2] : tsc[3];
+      if (VAN) van[base + x] = lane == 0 ? vsc[0] : lane == 1 ? vsc[1] : lane == 2 ? vsc[2] : vsc[3];
+    }
+  }
+}
+
+}  // namespace ipv

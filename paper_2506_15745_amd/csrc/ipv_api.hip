@@ -7,6 +7,7 @@
 #include <cstdint>
 
 #include "../../include/ipv.h"
+#include "ipv_adjacent.hpp"
 #include "ipv_compact.hpp"
 #include "ipv_scores.hpp"
 #include "ipv_select.hpp"
@@ -24,6 +25,7 @@ namespace {
 constexpr int32_t kMaxRows = 65536;  // select: 1024 threads x 64 row flags
 constexpr int64_t kMaxWindowRows = 65536;        // r * p: recent rows scanned per table block
 constexpr int32_t kMaxRecentFrames = 256;
+static_assert(kPrevMaxPositions >= kPoolCells, "the prev-row walk holds one entry per patch position");
 constexpr int kCompactThreads = 512;
 constexpr int kCompactRows = 256;      // rows per compaction chunk
 constexpr int kCompactColBytes = 256;  // largest column block a compaction walk copies
@@ -56,8 +58,12 @@ ipv_status check_shape(const ipv_shape* s, Dims* d) {
   d->dtype = s->dtype;
   d->elem = s->dtype == IPV_BF16 ? 2 : 4;
   if (d->slices > (int64_t)INT32_MAX / 8) return IPV_ERR_SHAPE;
+  // buffer loads address one slice's rows with 32-bit byte offsets
+  if (d->S * d->D * d->elem > (int64_t)UINT32_MAX - 16) return IPV_ERR_SHAPE;
   return IPV_OK;
 }
+
+ipv_status check_mode(uint32_t mode) { return (mode & ~(uint32_t)IPV_MODE_ALL) ? IPV_ERR_ARG : IPV_OK; }
 
 ipv_status check_rows(const Dims& d, int32_t n) {
   if (n < 1 || n > d.S || n > kMaxRows) return IPV_ERR_SHAPE;
@@ -78,7 +84,9 @@ ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
 
 // ------------------------------------------------------------ workspace layout
 // [0, 256)                 device error word (uint32) + padding
-// table  slices * p * D    fp32 m_q vectors of the recent window
+// table  slices * p * D    fp32 m_q vectors of the recent window; in the
+//                          consecutive-frame TaR mode the same region holds
+//                          prev(x) per row instead (slices * S int32)
 // first  slices            int32 first recent row of each slice
 // pool   B * L             int32 pooling window per (stream, layer)
 // flags  walks * chunks    uint32 per compaction chunk (1 once its rows are loaded)
@@ -86,7 +94,9 @@ size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 int64_t compact_parts(const Dims& d) { return 2 * std::max<int64_t>(1, d.D * d.elem / kCompactColBytes) + 1; }
 int64_t max_chunks(const Dims& d) { return (d.S + kCompactRows - 1) / kCompactRows; }
 size_t table_offset() { return kWsHeader; }
-size_t table_bytes(const Dims& d) { return (size_t)(d.slices * d.p * d.D) * sizeof(float); }
+size_t table_bytes(const Dims& d) {
+  return std::max((size_t)(d.slices * d.p * d.D) * sizeof(float), (size_t)(d.slices * d.S) * sizeof(int32_t));
+}
 size_t first_offset(const Dims& d) { return up256(table_offset() + table_bytes(d)); }
 size_t pool_offset(const Dims& d) { return up256(first_offset(d) + (size_t)d.slices * sizeof(int32_t)); }
 size_t flags_offset(const Dims& d) { return up256(pool_offset(d) + (size_t)(d.B * d.L) * sizeof(int32_t)); }
@@ -103,6 +113,7 @@ ipv_status check_ws(const Dims& d, const void* ws, size_t ws_bytes) {
 
 uint32_t* err_word(void* ws) { return reinterpret_cast<uint32_t*>(ws); }
 float* ws_table(void* ws) { return reinterpret_cast<float*>(static_cast<char*>(ws) + table_offset()); }
+int32_t* ws_prev(void* ws) { return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + table_offset()); }
 int32_t* ws_first(void* ws, const Dims& d) {
   return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + first_offset(d));
 }
@@ -123,18 +134,39 @@ ipv_status no_mark() { return IPV_OK; }
 // between(): runs after the recent-key table is enqueued, before the sweep
 // zero_chunks > 0: the table kernel also zeroes the compaction flags for a
 // compaction of zero_chunks chunks per walk that follows in the same pass.
+// adjacent: consecutive-frame TaR (prev-row kernel, then the adjacent sweep,
+// with VaN fused into it when V is given)
 template <typename T, int D, typename Between>
 ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
                       int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between,
-                      int64_t zero_chunks) {
+                      int64_t zero_chunks, bool adjacent) {
   const bool do_tar = K != nullptr, do_van = V != nullptr;
+  uint32_t* zero = zero_chunks > 0 ? ws_flags(ws, d) : nullptr;
+  const int32_t zero_per_slice = (int32_t)(compact_parts(d) * zero_chunks);
+  if (do_tar && adjacent) {
+    k_prev_rows<<<dim3((uint32_t)d.slices), dim3(kPrevThreads), 0, st>>>(
+        fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws), zero, zero_per_slice);
+    IPV_TRY(between());
+    constexpr int ROWS = 256 / (D / Lane<T>::EPL) * 4;
+    const int32_t bps = (n + ROWS - 1) / ROWS;
+    const uint32_t work = (uint32_t)(d.slices * bps);
+    const T* k = static_cast<const T*>(K);
+    const T* v = static_cast<const T*>(V);
+    if (do_van)
+      k_adjacent_sweep<T, D, true><<<dim3(pad8(work)), dim3(256), 0, st>>>(k, v, ws_prev(ws), d.S, n,
+                                                                         ws_first(ws, d), tar, van, bps, work);
+    else
+      k_adjacent_sweep<T, D, false><<<dim3(pad8(work)), dim3(256), 0, st>>>(k, k, ws_prev(ws), d.S, n,
+                                                                          ws_first(ws, d), tar, van, bps, work);
+    return launched();
+  }
   if (do_tar) {
     constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
     const int32_t blocks = (int32_t)((d.p + GROUPS - 1) / GROUPS);
     const size_t lds = (size_t)GROUPS * r * sizeof(int32_t);
     k_recent_table<T, D><<<dim3((uint32_t)(d.slices * blocks)), dim3(256), lds, st>>>(
         static_cast<const T*>(K), fr, pa, d.S, n, r, (int32_t)d.p, blocks, ws_table(ws), ws_first(ws, d),
-        err_word(ws), zero_chunks > 0 ? ws_flags(ws, d) : nullptr, (int32_t)(compact_parts(d) * zero_chunks));
+        err_word(ws), zero, zero_per_slice);
   }
   IPV_TRY(between());
   using C = SweepCfg<T, D>;
@@ -160,9 +192,10 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
 template <typename Between = ipv_status (*)()>
 ipv_status scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
                   int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between = no_mark,
-                  int64_t zero_chunks = 0) {
-#define IPV_SCORES(T, DD) \
-  if (d.D == DD) return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between, zero_chunks);
+                  int64_t zero_chunks = 0, bool adjacent = false) {
+#define IPV_SCORES(T, DD)                                                                                        \
+  if (d.D == DD)                                                                                                 \
+    return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between, zero_chunks, adjacent);
   if (d.dtype == IPV_BF16) {
     IPV_SCORES(uint16_t, 32) IPV_SCORES(uint16_t, 64) IPV_SCORES(uint16_t, 128) IPV_SCORES(uint16_t, 256)
   } else {
@@ -188,27 +221,33 @@ __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t v) {
 
 constexpr int kSelThreads = 1024;
 
+// mode: the reverse bits complement a stage's keys; IPV_HEAD_SHARED gives one
+// block (and one keep set) to each (stream, layer)
 template <int RPT>
 ipv_status run_select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
-                      int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st) {
+                      int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st, uint32_t mode) {
+  const int32_t heads = (mode & IPV_HEAD_SHARED) ? (int32_t)d.H : 1;
+  const uint32_t tflip = (mode & IPV_TAR_REVERSE) ? 0xffffffffu : 0u;
+  const uint32_t vflip = (mode & IPV_VAN_REVERSE) ? 0xffffffffu : 0u;
+  const dim3 grid((uint32_t)(d.slices / heads));
   // 16-byte row-run loads need every slice to start 16-byte aligned
   if (d.S % 4 == 0)
-    k_select<kSelThreads, RPT, true><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(
-        tar, van, fr, d.S, n, budget, tar_total, r, keep, err);
+    k_select<kSelThreads, RPT, true><<<grid, dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget, tar_total, r,
+                                                                         keep, err, heads, tflip, vflip);
   else
-    k_select<kSelThreads, RPT, false><<<dim3((uint32_t)d.slices), dim3(kSelThreads), 0, st>>>(
-        tar, van, fr, d.S, n, budget, tar_total, r, keep, err);
+    k_select<kSelThreads, RPT, false><<<grid, dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget, tar_total,
+                                                                          r, keep, err, heads, tflip, vflip);
   return launched();
 }
 
 ipv_status select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
-                  int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st) {
+                  int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st, uint32_t mode) {
   const int32_t rpt = (n + kSelThreads - 1) / kSelThreads;
-  if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
-  if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
-  if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
-  if (rpt <= 32) return run_select<32>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
-  return run_select<64>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st);
+  if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
+  if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
+  if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
+  if (rpt <= 32) return run_select<32>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
+  return run_select<64>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
 }
 
 int64_t compact_chunks(int32_t budget) { return (budget + kCompactRows - 1) / kCompactRows; }
@@ -287,17 +326,18 @@ ipv_status ipv_workspace_bytes(const ipv_shape* shape, size_t* bytes) {
 }
 
 ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* frame_idx, const int32_t* patch_idx,
-                          int32_t n_tokens, int32_t recent_frames, float* tar, void* ws, size_t ws_bytes,
-                          void* stream) {
+                          int32_t n_tokens, int32_t recent_frames, uint32_t mode, float* tar, void* ws,
+                          size_t ws_bytes, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
   if (!K || !frame_idx || !patch_idx || !tar) return IPV_ERR_NULL;
   if (!aligned(K, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) || !aligned(tar, 16)) return IPV_ERR_ALIGN;
   IPV_TRY(check_rows(d, n_tokens));
   IPV_TRY(check_recent(d, recent_frames));
+  IPV_TRY(check_mode(mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
   return scores(d, K, nullptr, frame_idx, patch_idx, n_tokens, recent_frames, tar, nullptr, ws,
-                static_cast<hipStream_t>(stream));
+                static_cast<hipStream_t>(stream), no_mark, 0, (mode & IPV_TAR_ADJACENT) != 0);
 }
 
 ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* frame_idx, const int32_t* patch_idx,
@@ -323,8 +363,8 @@ ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* 
 }
 
 ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van, const int32_t* frame_idx,
-                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, int32_t* keep_idx,
-                      void* ws, size_t ws_bytes, void* stream) {
+                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                      int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
   if (!tar || !van || !frame_idx || !keep_idx) return IPV_ERR_NULL;
@@ -333,9 +373,10 @@ ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van
   IPV_TRY(check_recent(d, recent_frames));
   if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
   IPV_TRY(check_budget(d, n_tokens, budget, recent_frames));
+  IPV_TRY(check_mode(mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
   return select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
-                err_word(ws), static_cast<hipStream_t>(stream));
+                err_word(ws), static_cast<hipStream_t>(stream), mode);
 }
 
 ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
@@ -354,7 +395,7 @@ ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_
 }
 
 ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                              int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                              int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
                               const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
                               size_t ws_bytes, void* stream, const ipv_events* events) {
   Dims d;
@@ -368,6 +409,7 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
   if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
   IPV_TRY(check_budget(d, n_tokens, budget, recent_frames));
   IPV_TRY(check_tau(cv_tau));
+  IPV_TRY(check_mode(mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
   hipStream_t st = static_cast<hipStream_t>(stream);
   auto mark = [&](int i) -> ipv_status {
@@ -376,22 +418,23 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
   };
   IPV_TRY(mark(0));
   IPV_TRY(scores(d, K, V, frame_idx, patch_idx, n_tokens, recent_frames, tar, van, ws, st,
-                 [&]() { return mark(1); }, compact_chunks(budget)));
+                 [&]() { return mark(1); }, compact_chunks(budget), (mode & IPV_TAR_ADJACENT) != 0));
   IPV_TRY(mark(2));
   if (cv_tau) IPV_TRY(pool_d(d, cv_tau, van, frame_idx, patch_idx, n_tokens, nullptr, ws, st));
   IPV_TRY(mark(3));
   IPV_TRY(select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
-                 err_word(ws), st));
+                 err_word(ws), st, mode));
   IPV_TRY(mark(4));
   IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, st, true));
   return mark(5);
 }
 
 ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, const double* cv_tau,
-                        float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream) {
-  return ipv_compress_timed(shape, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar,
-                            van, keep_idx, ws, ws_bytes, stream, nullptr);
+                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                        const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
+                        void* stream) {
+  return ipv_compress_timed(shape, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, mode, cv_tau,
+                            tar, van, keep_idx, ws, ws_bytes, stream, nullptr);
 }
 
 ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
@@ -417,7 +460,7 @@ ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_i
 ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                         int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
                         int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
-                        const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
+                        uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
                         int32_t* n_out, int32_t* compressed, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
@@ -434,13 +477,14 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
     if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
     IPV_TRY(check_budget(d, n1, budget, recent_frames));
     IPV_TRY(check_tau(cv_tau));
+    IPV_TRY(check_mode(mode));
     IPV_TRY(check_ws(d, ws, ws_bytes));
   }
   IPV_TRY(ipv_append(shape, K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, rows, frame_id, first_patch, stream));
   *n_out = n1;
   *compressed = 0;
   if (n1 < mem_cap) return IPV_OK;
-  IPV_TRY(ipv_compress(shape, K, V, frame_idx, patch_idx, n1, budget, alpha, recent_frames, cv_tau, tar, van,
+  IPV_TRY(ipv_compress(shape, K, V, frame_idx, patch_idx, n1, budget, alpha, recent_frames, mode, cv_tau, tar, van,
                        keep_idx, ws, ws_bytes, stream));
   *n_out = budget;
   *compressed = 1;

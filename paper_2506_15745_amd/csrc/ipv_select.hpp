@@ -1,5 +1,12 @@
 // Keep-set selection (Algorithm 1 steps (3)-(5); Sec. 3.3), one workgroup of
-// NT threads per (stream, layer, head) slice.
+// NT threads per (stream, layer, head) slice, or per (stream, layer) when the
+// heads share one keep set.
+//
+// Variants: a reversed stage (the TaR Reverse / VaN Reverse rows of Tab. 5)
+// complements its keys, so the same top-k takes the lowest scores, ties still
+// to the lowest rows. Head-shared selection ranks, per row, the fp32 sum of
+// the layer's head scores taken in head order, checks that every head holds
+// the same frame ids, and writes the one keep set to every head.
 //
 // Thread t owns the RPT consecutive rows [t*RPT, (t+1)*RPT). All of its frame
 // ids and both score columns are loaded at once (16-byte buffer loads),
@@ -211,26 +218,71 @@ __device__ __forceinline__ void load_row_run(const void* __restrict__ col, int64
   }
 }
 
-// One slice with NT threads. VEC: every slice's row 0 is 16-byte aligned
-// (capacity % 4 == 0) so row runs load 16 bytes at a time.
+// A score run summed over `heads` consecutive slices (column stride S) in
+// fp32, head 0 first, starting from +0 (the order the keep decision is
+// defined in); heads == 1 is the slice's own run.
+template <int RPT, bool VEC>
+__device__ __forceinline__ void load_score_run(const float* __restrict__ col, int64_t S, int32_t heads, int64_t row0,
+                                               uint32_t (&out)[RPT]) {
+  load_row_run<RPT, VEC>(col, S, row0, out);
+  if (heads == 1) return;
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) out[i] = __float_as_uint(0.f + __uint_as_float(out[i]));
+#pragma unroll 1
+  for (int32_t h = 1; h < heads; ++h) {
+    uint32_t t[RPT];
+    load_row_run<RPT, VEC>(col + h * S, S, row0, t);
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) out[i] = __float_as_uint(__uint_as_float(out[i]) + __uint_as_float(t[i]));
+  }
+}
+
+// Head-shared selection: true if some head's frame ids differ from head 0's
+// on this thread's rows.
+template <int RPT, bool VEC>
+__device__ __forceinline__ bool heads_differ(const int32_t* __restrict__ fr0, int64_t S, int32_t heads, int64_t row0,
+                                             int32_t n, const uint32_t (&fr)[RPT]) {
+  bool diff = false;
+#pragma unroll 1
+  for (int32_t h = 1; h < heads; ++h) {
+    uint32_t t[RPT];
+    load_row_run<RPT, VEC>(fr0 + h * S, S, row0, t);
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) diff |= row0 + i < n && t[i] != fr[i];
+  }
+  return diff;
+}
+
+// One group of `heads` slices (1: a slice of its own) with NT threads. VEC:
+// every slice's row 0 is 16-byte aligned (capacity % 4 == 0) so row runs
+// load 16 bytes at a time. tflip / vflip: 0, or ~0 for a reversed stage.
 template <int NT, int RPT, bool VEC>
 __device__ __forceinline__ void select_slice(const float* __restrict__ tar, const float* __restrict__ van,
                              const int32_t* __restrict__ frame_idx, int64_t S, int32_t n, int32_t budget,
                              int32_t tar_total, int32_t r, int32_t* __restrict__ keep_idx,
-                             uint32_t* err, int64_t slice, SelShared<NT>& sh) {
+                             uint32_t* err, int64_t slice, int32_t heads, uint32_t tflip, uint32_t vflip,
+                             SelShared<NT>& sh) {
   constexpr int NW = NT / kWave;
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int64_t base = slice * S;
   const int64_t row0 = (int64_t)tid * RPT;
   int32_t* keep = keep_idx + slice * budget;
+  // every head of the group gets the same keep set
+  auto put = [&](int32_t j, int32_t row) {
+    if (heads == 1) {
+      keep[j] = row;
+      return;
+    }
+    for (int32_t h = 0; h < heads; ++h) keep[(int64_t)h * budget + j] = row;
+  };
 
   // all loads are issued up front; with many rows per thread the VaN column
   // waits until the TaR stage is done, to stay within the register budget
   constexpr bool kEarlyVan = RPT <= 16;
   uint32_t fr[RPT], kt[RPT], kv[RPT];
   load_row_run<RPT, VEC>(frame_idx + base, S, row0, fr);
-  load_row_run<RPT, VEC>(tar + base, S, row0, kt);
-  if (kEarlyVan) load_row_run<RPT, VEC>(van + base, S, row0, kv);
+  load_score_run<RPT, VEC>(tar + base, S, heads, row0, kt);
+  if (kEarlyVan) load_score_run<RPT, VEC>(van + base, S, heads, row0, kv);
   const __amdgpu_buffer_rsrc_t frs = buffer_rsrc(frame_idx + base, (uint32_t)(S * 4));
   const int32_t last = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)(n - 1) * 4u, 0, 0);
   const int32_t prev_row = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)max(row0 - 1, (int64_t)0) * 4u,
@@ -241,7 +293,8 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   const int64_t thr = (int64_t)last - r + 1;
   uint64_t valid = 0, recent = 0;
   int32_t prev = before;
-  bool bad = false, nan_t = false, nan_v = false;
+  bool bad = heads > 1 && heads_differ<RPT, VEC>(frame_idx + base, S, heads, row0, n, fr);
+  bool nan_t = false, nan_v = false;
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     if (row0 + i < n) {
@@ -258,8 +311,8 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
       nan_t |= !rec && __uint_as_float(kt[i]) != __uint_as_float(kt[i]);
       if (kEarlyVan) nan_v |= !rec && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
     }
-    kt[i] = order_key(__uint_as_float(kt[i]));
-    if (kEarlyVan) kv[i] = order_key(__uint_as_float(kv[i]));
+    kt[i] = order_key(__uint_as_float(kt[i])) ^ tflip;
+    if (kEarlyVan) kv[i] = order_key(__uint_as_float(kv[i])) ^ vflip;
   }
   const uint64_t past = valid & ~recent;
   // key ranges of both stages over the past rows, and the frame check
@@ -300,7 +353,7 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   if (broken) {
     // metadata breaks the cache invariants: report, and keep rows 0..C-1 in place
     if (tid == 0) raise_error(err, any_bad ? 2u : 4u);
-    for (int32_t j = tid; j < budget; j += NT) keep[j] = j;
+    for (int32_t j = tid; j < budget; j += NT) put(j, j);
     return;
   }
   const int32_t b_tar = max(0, tar_total - n_recent);
@@ -315,11 +368,11 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   if (b_van > 0) {
     const uint64_t cand = past & ~pick_t;
     if (!kEarlyVan) {
-      load_row_run<RPT, VEC>(van + base, S, row0, kv);
+      load_score_run<RPT, VEC>(van + base, S, heads, row0, kv);
 #pragma unroll
       for (int i = 0; i < RPT; ++i) {
         nan_v |= ((past >> i) & 1ull) && __uint_as_float(kv[i]) != __uint_as_float(kv[i]);
-        kv[i] = order_key(__uint_as_float(kv[i]));
+        kv[i] = order_key(__uint_as_float(kv[i])) ^ vflip;
       }
       block_min_max<NT, RPT>(kv, cand, sh, vmn, vmx);
     }
@@ -333,16 +386,19 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   if (total != budget && tid == 0) raise_error(err, 16u);  // only reachable with NaN keys
 #pragma unroll
   for (int i = 0; i < RPT; ++i)
-    if (((kept >> i) & 1ull) && pos < budget) keep[pos++] = (int32_t)(row0 + i);
+    if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
 }
 
+// grid: one block per group of `heads` consecutive slices
 template <int NT, int RPT, bool VEC>
 __global__ __launch_bounds__(NT) void k_select(const float* __restrict__ tar, const float* __restrict__ van,
                                                const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
                                                int32_t budget, int32_t tar_total, int32_t r,
-                                               int32_t* __restrict__ keep_idx, uint32_t* err) {
+                                               int32_t* __restrict__ keep_idx, uint32_t* err, int32_t heads,
+                                               uint32_t tflip, uint32_t vflip) {
   __shared__ SelShared<NT> sh;
-  select_slice<NT, RPT, VEC>(tar, van, frame_idx, S, n, budget, tar_total, r, keep_idx, err, blockIdx.x, sh);
+  select_slice<NT, RPT, VEC>(tar, van, frame_idx, S, n, budget, tar_total, r, keep_idx, err,
+                             (int64_t)blockIdx.x * heads, heads, tflip, vflip, sh);
 }
 
 }  // namespace ipv

@@ -27,6 +27,8 @@ LIB_PATH = os.path.join(HERE, "libipv.so")
 OK, ERR_NULL, ERR_ALIGN, ERR_SHAPE, ERR_DTYPE, ERR_BUDGET, ERR_ARG, ERR_WORKSPACE, ERR_HIP = range(9)
 BF16, F32 = 0, 1
 DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN, DEV_WAIT_TIMEOUT = 1, 2, 4, 8, 16, 32
+# `mode` bits: reversed TaR / VaN stages, consecutive-frame TaR, head-shared selection
+TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED = 1, 2, 4, 8
 
 EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
            "ipv_compress", "ipv_compress_timed", "ipv_append", "ipv_ckv_step", "ipv_clear_device_errors",
@@ -67,15 +69,16 @@ def lib() -> ctypes.CDLL:
         vp, i32, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_double, ctypes.c_size_t
         sp = ctypes.POINTER(Shape)
         L.ipv_workspace_bytes.argtypes = [sp, ctypes.POINTER(ctypes.c_size_t)]
-        L.ipv_tar_scores.argtypes = [sp, vp, vp, vp, i32, i32, vp, vp, sz, vp]
+        u32 = ctypes.c_uint32
+        L.ipv_tar_scores.argtypes = [sp, vp, vp, vp, i32, i32, u32, vp, vp, sz, vp]
         L.ipv_van_scores.argtypes = [sp, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
-        L.ipv_select.argtypes = [sp, vp, vp, vp, i32, i32, f64, i32, vp, vp, sz, vp]
+        L.ipv_select.argtypes = [sp, vp, vp, vp, i32, i32, f64, i32, u32, vp, vp, sz, vp]
         L.ipv_compact.argtypes = [sp, vp, vp, vp, vp, i32, vp, i32, vp, sz, vp]
-        L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, vp, vp, vp, vp, vp, sz, vp]
-        L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, vp, vp, vp, vp, vp, sz, vp,
+        L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp]
+        L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp,
                                          ctypes.POINTER(Events)]
         L.ipv_append.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, vp]
-        L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f64, i32, vp, vp, vp,
+        L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f64, i32, u32, vp, vp, vp,
                                    vp, vp, sz, ctypes.POINTER(i32), ctypes.POINTER(i32), vp]
         L.ipv_clear_device_errors.argtypes = [vp, sz, vp]
         L.ipv_read_device_errors.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
@@ -138,10 +141,11 @@ def alloc_workspace(shape: Shape, device) -> torch.Tensor:
     return torch.zeros(workspace_bytes(shape), dtype=torch.uint8, device=device)
 
 
-def ipv_tar_scores(K, frame_idx, patch_idx, n_tokens, recent_frames, tar, ws, grid_h, grid_w, stream=None):
+def ipv_tar_scores(K, frame_idx, patch_idx, n_tokens, recent_frames, tar, ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
     _check(lib().ipv_tar_scores(ctypes.byref(s), _ptr(K), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
-                                recent_frames, _ptr(tar), _ptr(ws), ws.numel(), _stream(stream)), "ipv_tar_scores")
+                                recent_frames, mode, _ptr(tar), _ptr(ws), ws.numel(), _stream(stream)),
+           "ipv_tar_scores")
 
 
 def ipv_van_scores(V, frame_idx, patch_idx, n_tokens, cv_tau, van, pool_size, ws, grid_h, grid_w, stream=None):
@@ -153,13 +157,14 @@ def ipv_van_scores(V, frame_idx, patch_idx, n_tokens, cv_tau, van, pool_size, ws
 
 
 def ipv_select(tar, van, frame_idx, n_tokens, budget, alpha, recent_frames, keep_idx, ws, grid_h, grid_w,
-               head_dim=128, dtype=BF16, stream=None):
+               head_dim=128, dtype=BF16, stream=None, mode=0):
     """The select step needs only the slice geometry: (B, L, H, S) from the
     score tensors and the patch grid; head_dim/dtype only size the workspace."""
     B, L, H, S = tar.shape
     s = Shape(B, L, H, head_dim, S, grid_h, grid_w, dtype)
     _check(lib().ipv_select(ctypes.byref(s), _ptr(tar), _ptr(van), _ptr(frame_idx), n_tokens, budget,
-                            float(alpha), recent_frames, _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream)),
+                            float(alpha), recent_frames, mode, _ptr(keep_idx), _ptr(ws), ws.numel(),
+                            _stream(stream)),
            "ipv_select")
 
 
@@ -171,21 +176,21 @@ def ipv_compact(K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, grid
 
 
 def ipv_compress(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van, keep_idx,
-                 ws, grid_h, grid_w, stream=None):
+                 ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
-                              budget, float(alpha), recent_frames, None if tau is None else ctypes.addressof(tau),
+                              budget, float(alpha), recent_frames, mode, None if tau is None else ctypes.addressof(tau),
                               _ptr(tar), _ptr(van), _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream)),
            "ipv_compress")
 
 
 def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van,
-                       keep_idx, ws, grid_h, grid_w, events: Events, stream=None):
+                       keep_idx, ws, grid_h, grid_w, events: Events, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_compress_timed(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
-                                    budget, float(alpha), recent_frames,
+                                    budget, float(alpha), recent_frames, mode,
                                     None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
                                     _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(events)),
            "ipv_compress_timed")
@@ -206,7 +211,7 @@ def ipv_append(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, fir
 
 
 def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, first_patch, mem_cap, budget,
-                 alpha, recent_frames, cv_tau, tar, van, keep_idx, ws, grid_h, grid_w, stream=None):
+                 alpha, recent_frames, cv_tau, tar, van, keep_idx, ws, grid_h, grid_w, stream=None, mode=0):
     """Append, then compress to `budget` once the cache holds >= mem_cap rows.
     Returns (new row count, whether the pass ran)."""
     s = shape_of(K, grid_h, grid_w)
@@ -217,7 +222,8 @@ def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, f
     n_out, comp = ctypes.c_int32(0), ctypes.c_int32(0)
     _check(lib().ipv_ckv_step(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
                               _ptr(K_new), _ptr(V_new), K_new.shape[3], frame_id, first_patch, mem_cap, budget,
-                              float(alpha), recent_frames, None if tau is None else ctypes.addressof(tau), _ptr(tar),
+                              float(alpha), recent_frames, mode, None if tau is None else ctypes.addressof(tau),
+                              _ptr(tar),
                               _ptr(van), _ptr(keep_idx), _ptr(ws), 0 if ws is None else ws.numel(),
                               ctypes.byref(n_out), ctypes.byref(comp), _stream(stream)), "ipv_ckv_step")
     return n_out.value, bool(comp.value)
@@ -251,9 +257,10 @@ class Compressor:
         self.keep_idx = torch.zeros((B, L, H, budget), dtype=torch.int32, device=dev)
         self.ws = alloc_workspace(self.shape, dev)
 
-    def compress(self, K, V, frame_idx, patch_idx, n_tokens, alpha, recent_frames, cv_tau=None, stream=None):
+    def compress(self, K, V, frame_idx, patch_idx, n_tokens, alpha, recent_frames, cv_tau=None, stream=None,
+                 mode=0):
         ipv_compress(K, V, frame_idx, patch_idx, n_tokens, self.budget, alpha, recent_frames, cv_tau, self.tar,
-                     self.van, self.keep_idx, self.ws, self.grid_h, self.grid_w, stream)
+                     self.van, self.keep_idx, self.ws, self.grid_h, self.grid_w, stream, mode)
 
     def device_errors(self) -> int:
         return ipv_read_device_errors(self.ws)

@@ -118,3 +118,36 @@ def oracle_gather_equal(K0, V0, fr0, pa0, n, keep, got: GpuPass):
     assert np.array_equal(got.V[..., :C, :].view(np.uint8), Vo[..., :C, :].view(np.uint8)), "V compaction differs"
     assert np.array_equal(got.frame_idx[..., :C], fo[..., :C]), "frame_idx compaction differs"
     assert np.array_equal(got.patch_idx[..., :C], po[..., :C]), "patch_idx compaction differs"
+
+
+def oracle_mode(mode: int) -> int:
+    """The library's mode bits as the oracle's (the two define them separately)."""
+    pairs = ((ipv.TAR_REVERSE, oracle.TAR_REVERSE), (ipv.VAN_REVERSE, oracle.VAN_REVERSE),
+             (ipv.TAR_ADJACENT, oracle.TAR_ADJACENT), (ipv.HEAD_SHARED, oracle.HEAD_SHARED))
+    return sum(o for g, o in pairs if mode & g)
+
+
+def check_pass(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, got: GpuPass):
+    """Every rule above for one pass in any mode; K, V, fr, pa are the cache
+    before the pass. Returns the near-threshold row count."""
+    om = oracle_mode(mode)
+    tar64 = oracle.tar_scores(K, fr, pa, n, r, gh, gw, mode=om)
+    van64, _ = oracle.van_scores(V, fr, pa, n, gh, gw)
+    sel = oracle.select(tar64.astype(np.float32), van64.astype(np.float32), fr, n, budget, alpha, r, mode=om)
+    check_scores(got.tar, got.van, tar64, van64, n, name)
+    check_ascending(got.keep, n)
+    if mode & ipv.HEAD_SHARED:
+        # the decision is taken on the heads' summed scores: the rule's distances too
+        H = K.shape[2]
+        st = np.repeat(tar64.sum(axis=2, keepdims=True), H, axis=2)
+        sv = np.repeat(van64.sum(axis=2, keepdims=True), H, axis=2)
+        near = check_keep(got.keep, sel, st, sv)
+        assert np.array_equal(got.keep, np.repeat(got.keep[:, :, :1], H, axis=2)), "heads kept different rows"
+    else:
+        near = check_keep(got.keep, sel, tar64, van64)
+    oracle_gather_equal(K, V, fr, pa, n, got.keep, got)
+    # the oracle's decision on the GPU's own fp32 scores is the GPU's keep set
+    sel_g = oracle.select(np.ascontiguousarray(got.tar), np.ascontiguousarray(got.van), fr, n, budget, alpha, r,
+                          mode=om)
+    assert np.array_equal(sel_g.keep_idx, got.keep), "%s: keep set differs from the oracle's on the GPU scores" % name
+    return near

@@ -62,13 +62,13 @@ def test_workspace_size_covers_the_recent_table():
     assert e.value.status == ipv.ERR_DTYPE
 
 
-def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, ws=FAKE, wsb=None, K=FAKE):
+def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, ws=FAKE, wsb=None, K=FAKE, mode=0):
     p = dict(K=K, V=FAKE, fr=FAKE, pa=FAKE, tar=FAKE, van=FAKE, keep=FAKE)
     if ptrs:
         p.update(ptrs)
     t = None if tau is None else (ctypes.c_double * 3)(*tau)
     wsb = wsb if wsb is not None else 0  # default: workspace too small
-    return ipv.lib().ipv_compress(ctypes.byref(s), p["K"], p["V"], p["fr"], p["pa"], n, budget, alpha, r,
+    return ipv.lib().ipv_compress(ctypes.byref(s), p["K"], p["V"], p["fr"], p["pa"], n, budget, alpha, r, mode,
                                   None if t is None else ctypes.addressof(t), p["tar"], p["van"], p["keep"], ws,
                                   wsb, None)
 
@@ -91,6 +91,8 @@ def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, w
     (dict(ws=None), ipv.ERR_WORKSPACE),
     (dict(ws=FAKE + 16), ipv.ERR_ALIGN),
     (dict(), ipv.ERR_WORKSPACE),                  # ws_bytes = 0
+    (dict(mode=16, wsb=1 << 40), ipv.ERR_ARG),    # unknown mode bit
+    (dict(mode=0xffffffff, wsb=1 << 40), ipv.ERR_ARG),
 ])
 def test_compress_rejects_before_launch(case, status):
     assert call_compress(shape(), **case) == status
@@ -107,6 +109,12 @@ def test_bad_shapes(kw, status):
     assert call_compress(shape(**kw), wsb=1 << 40) == status
 
 
+def test_slice_bytes_beyond_32_bit_offsets_rejected():
+    # buffer loads address a slice with 32-bit byte offsets: S * D * elem must fit
+    s = shape(capacity=(1 << 22) + 1, head_dim=256, dtype=ipv.F32)
+    assert call_compress(s, wsb=1 << 50) == ipv.ERR_SHAPE
+
+
 def test_rows_above_select_limit_rejected():
     s = shape(capacity=70000)
     assert call_compress(s, n=70000, budget=35000, wsb=1 << 40) == ipv.ERR_SHAPE
@@ -115,14 +123,17 @@ def test_rows_above_select_limit_rejected():
 def test_entry_points_validate_their_own_arguments():
     L, s = ipv.lib(), shape()
     big = 1 << 40
-    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 0, FAKE, FAKE, big, None) == ipv.ERR_ARG
-    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, None, FAKE, 6272, 4, FAKE, FAKE, big, None) == ipv.ERR_NULL
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 0, 0, FAKE, FAKE, big, None) == ipv.ERR_ARG
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, None, FAKE, 6272, 4, 0, FAKE, FAKE, big, None) == ipv.ERR_NULL
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 4, 32, FAKE, FAKE, big, None) == ipv.ERR_ARG
     assert L.ipv_van_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, None, FAKE, FAKE + 2, FAKE, big,
                             None) == ipv.ERR_ALIGN
-    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 3136, -0.1, 4, FAKE, FAKE, big,
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 3136, -0.1, 4, 0, FAKE, FAKE, big,
                         None) == ipv.ERR_ARG
-    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 100, 0.5, 4, FAKE, FAKE, big,
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 100, 0.5, 4, 0, FAKE, FAKE, big,
                         None) == ipv.ERR_BUDGET
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 3136, 0.5, 4, 64, FAKE, FAKE, big,
+                        None) == ipv.ERR_ARG
     assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE, 0, None, 0, None) == ipv.ERR_BUDGET
     assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE + 4, 10, None, 0,
                          None) == ipv.ERR_ALIGN
@@ -152,9 +163,9 @@ def test_append_and_ckv_step_validate_before_launch():
     assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, 100, 0, 97, None) == ipv.ERR_ARG
     n_out, comp = ctypes.c_int32(), ctypes.c_int32()
 
-    def step(n=6076, rows=196, cap=6272, budget=3136, tar=FAKE, ws=FAKE, wsb=big, nout=True):
+    def step(n=6076, rows=196, cap=6272, budget=3136, tar=FAKE, ws=FAKE, wsb=big, nout=True, mode=0):
         return L.ipv_ckv_step(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, n, FAKE, FAKE, rows, 30, 0, cap, budget, 0.5,
-                              4, None, tar, FAKE, FAKE, ws, wsb, ctypes.byref(n_out) if nout else None,
+                              4, mode, None, tar, FAKE, FAKE, ws, wsb, ctypes.byref(n_out) if nout else None,
                               ctypes.byref(comp), None)
 
     assert step(nout=False) == ipv.ERR_NULL
@@ -164,3 +175,4 @@ def test_append_and_ckv_step_validate_before_launch():
     assert step(tar=None) == ipv.ERR_NULL         # the pass would run: its arguments are checked first
     assert step(wsb=0) == ipv.ERR_WORKSPACE
     assert step(budget=700) == ipv.ERR_BUDGET     # smaller than the recent window
+    assert step(mode=128) == ipv.ERR_ARG          # unknown mode bit

@@ -12,7 +12,7 @@ from tests import parity as P
 pytestmark = pytest.mark.gpu
 
 
-def run_loop(L, H, D, gh, gw, frames, cap, budget, r, alpha, dtype, seed, rho_spec):
+def run_loop(L, H, D, gh, gw, frames, cap, budget, r, alpha, dtype, seed, rho_spec, mode=0):
     p = gh * gw
     S = cap + p
     full = synth.fresh_cache(seed, L, H, frames * p, D, gh, gw, frames * p, dtype, rho_spec)
@@ -34,8 +34,9 @@ def run_loop(L, H, D, gh, gw, frames, cap, budget, r, alpha, dtype, seed, rho_sp
         before, n_prev = (Ko.copy(), Vo.copy(), fo.copy(), po.copy()), n
         n_gpu, fired = ipv.ipv_ckv_step(Kd, Vd, fd, pd, n_gpu, P.to_device(kn, kind), P.to_device(vn, kind), f, 0,
                                         cap, budget, alpha, r, None, comp.tar, comp.van, comp.keep_idx, comp.ws,
-                                        gh, gw)
-        n, out = oracle.ckv_step(Ko, Vo, fo, po, n, kn, vn, f, 0, cap, budget, alpha, r, gh, gw)
+                                        gh, gw, mode=mode)
+        n, out = oracle.ckv_step(Ko, Vo, fo, po, n, kn, vn, f, 0, cap, budget, alpha, r, gh, gw,
+                                 mode=P.oracle_mode(mode))
         assert n_gpu == n and fired == (out is not None), "frame %d" % f
         torch.cuda.synchronize()
         assert comp.device_errors() == 0
@@ -49,15 +50,9 @@ def run_loop(L, H, D, gh, gw, frames, cap, budget, r, alpha, dtype, seed, rho_sp
         # a pass ran on the appended cache: compare it like the single-pass parity tests
         Kb, Vb, fb, pb = before
         n_full = oracle.append(Kb, Vb, fb, pb, n_prev, kn, vn, f)
-        tar64 = oracle.tar_scores(Kb, fb, pb, n_full, r, gh, gw)
-        van64, _ = oracle.van_scores(Vb, fb, pb, n_full, gh, gw)
-        sel = oracle.select(tar64.astype(np.float32), van64.astype(np.float32), fb, n_full, budget, alpha, r)
-        g_tar, g_van, g_keep = comp.tar.cpu().numpy(), comp.van.cpu().numpy(), comp.keep_idx.cpu().numpy()
-        P.check_scores(g_tar, g_van, tar64, van64, n_full, "pass %d" % passes)
-        P.check_ascending(g_keep, n_full)
-        near += P.check_keep(g_keep, sel, tar64, van64)
-        got = P.GpuPass(g_tar, g_van, g_keep, P.to_host(Kd), P.to_host(Vd), fd.cpu().numpy(), pd.cpu().numpy(), 0)
-        P.oracle_gather_equal(Kb, Vb, fb, pb, n_full, g_keep, got)
+        got = P.GpuPass(comp.tar.cpu().numpy(), comp.van.cpu().numpy(), comp.keep_idx.cpu().numpy(), P.to_host(Kd),
+                        P.to_host(Vd), fd.cpu().numpy(), pd.cpu().numpy(), 0)
+        near += P.check_pass("pass %d" % passes, Kb, Vb, fb, pb, n_full, budget, alpha, r, gh, gw, mode, got)
         # teacher forcing: the oracle's state becomes the device state
         Kd.copy_(P.to_device(Ko, kind))
         Vd.copy_(P.to_device(Vo, kind))
@@ -68,14 +63,17 @@ def run_loop(L, H, D, gh, gw, frames, cap, budget, r, alpha, dtype, seed, rho_sp
     return passes
 
 
-@pytest.mark.parametrize("dtype,D,gh,gw,cap_frames,budget_extra,r", [
-    (synth.BF16, 64, 3, 4, 6, 2, 2),     # budget not a whole number of frames: appends overshoot the cap
-    (synth.F32, 32, 2, 5, 8, 0, 1),
-    (synth.BF16, 128, 4, 4, 5, 5, 3),
+@pytest.mark.parametrize("dtype,D,gh,gw,cap_frames,budget_extra,r,mode", [
+    (synth.BF16, 64, 3, 4, 6, 2, 2, 0),     # budget not a whole number of frames: appends overshoot the cap
+    (synth.F32, 32, 2, 5, 8, 0, 1, 0),
+    (synth.BF16, 128, 4, 4, 5, 5, 3, 0),
+    # the variants over many passes: gappy old frames, heads kept aligned
+    (synth.BF16, 128, 3, 4, 6, 2, 2, ipv.HEAD_SHARED | ipv.TAR_ADJACENT),
+    (synth.F32, 64, 2, 5, 8, 3, 1, ipv.TAR_ADJACENT | ipv.VAN_REVERSE),
 ])
-def test_ckv_loop_matches_oracle(dtype, D, gh, gw, cap_frames, budget_extra, r):
+def test_ckv_loop_matches_oracle(dtype, D, gh, gw, cap_frames, budget_extra, r, mode):
     p = gh * gw
     cap = cap_frames * p
     budget = max(r * p + 1, cap // 2) + budget_extra
-    passes = run_loop(2, 2, D, gh, gw, 24, cap, budget, r, 0.5, dtype, 41, synth.RhoSpec(0.0, 0.95))
+    passes = run_loop(2, 2, D, gh, gw, 24, cap, budget, r, 0.5, dtype, 41, synth.RhoSpec(0.0, 0.95), mode)
     assert passes >= 3

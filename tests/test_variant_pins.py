@@ -79,6 +79,13 @@ def test_adjacent_matches_dictionary_walk_on_fragmented_caches(seed):
     np.testing.assert_allclose(got, brute_adjacent(full[keep], frames, patches, n, r), rtol=1e-12, atol=1e-12)
 
 
+def test_adjacent_rejects_a_repeated_frame_patch_pair():
+    K, V, fr, pa, n = slice_cache([[1, 0], [0, 1], [1, 1], [2, 0]], None, 1, 2, [0, 0, 1, 1], [0, 1, 1, 1])
+    oracle.tar_scores(K, fr, pa, n, 1, 1, 2)  # the recent-window score does not look at it
+    with pytest.raises(oracle.OracleError):
+        oracle.tar_scores(K, fr, pa, n, 1, 1, 2, mode=oracle.TAR_ADJACENT)
+
+
 # ----------------------------------------------------------------- reversed stages
 
 def brute_bottom(scores, cands, b):
