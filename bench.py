@@ -9,6 +9,7 @@ inside it; a 1 GiB write and read evict the caches before warm-up and before
 timing. Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 7b-class-28L]
+                  [--mode tar_reverse,van_reverse,tar_adjacent,head_shared]
 """
 from __future__ import annotations
 
@@ -34,6 +35,18 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = os.path.join(ROOT, "paper_2506_15745_amd", "csrc")
 PEAK_HBM_GBPS = 8000.0
 STEP_NAMES = ("recent_table", "score_sweep", "pool", "select", "compact")
+# with consecutive-frame TaR the first two steps are the prev-row walk and the adjacent sweep
+STEP_NAMES_ADJACENT = ("prev_walk", "adjacent_sweep", "pool", "select", "compact")
+MODE_BITS = {"tar_reverse": 1, "van_reverse": 2, "tar_adjacent": 4, "head_shared": 8}
+
+
+def parse_mode(text: str) -> int:
+    bits = 0
+    for name in filter(None, text.split(",")):
+        if name not in MODE_BITS:
+            raise SystemExit("unknown mode %r (known: %s)" % (name, ", ".join(MODE_BITS)))
+        bits |= MODE_BITS[name]
+    return bits
 
 
 class Hip:
@@ -69,7 +82,7 @@ def make_cache(w: W.Workload):
     return st("K"), st("V"), st("frame_idx"), st("patch_idx")
 
 
-def cpu_baseline(w, K, V, fr, pa, alpha, seconds):
+def cpu_baseline(w, K, V, fr, pa, alpha, seconds, mode=0):
     """The CPU oracle on the same workload, on this host's cores."""
     import oracle
     # whole passes on fresh copies of the cache (the pass is in place) until
@@ -81,7 +94,7 @@ def cpu_baseline(w, K, V, fr, pa, alpha, seconds):
             np.copyto(dst, src)
         t = time.perf_counter()
         oracle.compress_inplace(Kc, Vc, fc, pc, w.n_tokens, w.budget, alpha, w.recent_frames, w.grid_h, w.grid_w,
-                                w.cv_tau)
+                                w.cv_tau, mode)
         times.append(time.perf_counter() - t)
     t = statistics.median(times)
     return {"value": round(w.algorithmic_bytes() / t / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
@@ -193,6 +206,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=W.SEVEN_B.name)
     ap.add_argument("--alpha", type=float, default=None)
+    ap.add_argument("--mode", default="", help="comma-separated variant modes (default: the method as published)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
@@ -221,6 +235,8 @@ def main():
 
     w = W.BY_NAME[args.workload]
     alpha = w.alphas[0] if args.alpha is None else args.alpha
+    mode = parse_mode(args.mode)
+    names = STEP_NAMES_ADJACENT if mode & MODE_BITS["tar_adjacent"] else STEP_NAMES
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     hip = Hip()
@@ -264,10 +280,11 @@ def main():
         Kd, Vd, fd, pd = replicas[i]
         if timed_kernels:
             ipv.ipv_compress_timed(Kd, Vd, fd, pd, w.n_tokens, w.budget, alpha, w.recent_frames, w.cv_tau,
-                                   comp.tar, comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w, ev_structs[i])
+                                   comp.tar, comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w, ev_structs[i],
+                                   mode=mode)
         else:
             ipv.ipv_compress(Kd, Vd, fd, pd, w.n_tokens, w.budget, alpha, w.recent_frames, w.cv_tau, comp.tar,
-                             comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w)
+                             comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w, mode=mode)
 
     evict(1.0)
     for i in range(args.warmup):
@@ -289,7 +306,7 @@ def main():
     timed = range(args.warmup + args.steps, reps)
     pass_us = [hip.elapsed_ms(events[i][0], events[i][5]) * 1e3 for i in timed]
     step_us = {name: statistics.mean(hip.elapsed_ms(events[i][k], events[i][k + 1]) * 1e3 for i in timed)
-               for k, name in enumerate(STEP_NAMES)}
+               for k, name in enumerate(names)}
 
     ms_per_step = wall / args.steps * 1e3
     algo = w.algorithmic_bytes()
@@ -300,9 +317,9 @@ def main():
     if w.n_tokens % w.p:
         n_recent = (w.recent_frames - 1) * w.p + w.n_tokens % w.p
     algo_by_step = {"recent_table": B * L * H * n_recent * row,
-                    "score_sweep": B * L * H * (2 * w.n_tokens - n_recent) * row,
+                    names[1]: B * L * H * (2 * w.n_tokens - n_recent) * row,
                     "compact": B * L * H * 4 * w.budget * row}
-    dom = max(("score_sweep", "compact"), key=lambda k: step_us[k])
+    dom = max((names[1], "compact"), key=lambda k: step_us[k])
     achieved = algo_by_step[dom] / (step_us[dom] * 1e-6) / 1e9
 
     out = {
@@ -320,7 +337,8 @@ def main():
         "data": "synthetic (seeded AR(1) keys, log-normal-scaled values)",
         "config": {"workload": w.name, "streams": B, "layers": L, "kv_heads": H, "head_dim": w.head_dim,
                    "tokens_per_frame": w.p, "n_tokens": w.n_tokens, "budget": w.budget,
-                   "recent_frames": w.recent_frames, "alpha": alpha, "parallelism": "single GPU"},
+                   "recent_frames": w.recent_frames, "alpha": alpha, "parallelism": "single GPU",
+                   **({"mode": args.mode} if mode else {})},
         "latency_us": {"wall_mean": round(ms_per_step * 1e3, 2), "events_p50": round(pct(pass_us, 0.5), 2),
                        "events_p99": round(pct(pass_us, 0.99), 2)},
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
@@ -335,7 +353,7 @@ def main():
         "device_errors": errors,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, K, V, fr, pa, alpha, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, K, V, fr, pa, alpha, args.cpu_seconds, mode)
     print(json.dumps(out), flush=True)
 
 

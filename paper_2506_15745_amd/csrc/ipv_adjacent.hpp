@@ -28,6 +28,9 @@ constexpr int kPrevMaxPositions = 8192;
 // frame id that decreases, or a patch id outside [0, p), sets an error bit;
 // such metadata gives no defined prev.
 //
+// A walk reads 16 patch ids per step with four aligned 16-byte LDS reads and
+// tests them all before it branches, so a step costs one LDS round trip.
+//
 // The chunk metadata is double-buffered, so one chunk costs two barriers:
 // (A) the chunk's metadata is visible, (B) every walk has read `last` and the
 // carry; then `last` and the carry are updated for the next chunk.
@@ -39,7 +42,8 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
                                                             uint32_t* __restrict__ zero, int32_t zero_per_slice) {
   constexpr int NT = kPrevThreads;
   __shared__ int32_t last[kPrevMaxPositions];
-  __shared__ int32_t cpa[2][NT], cfr[2][NT];
+  __shared__ alignas(16) int32_t cpa[2][NT];
+  __shared__ int32_t cfr[2][NT];
   // carry: frame id of the previous chunk's last row, and the row its frame starts at
   __shared__ int32_t carry_frame, carry_start;
   const int tid = threadIdx.x;
@@ -79,22 +83,27 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
       if (q < 0 || q >= p) {
         ebits |= 1u;
       } else {
-        const int32_t* pa = cpa[b];
-        int y = tid - 1, hit = -1;
-        while (y >= 3) {
-          const int32_t a0 = pa[y], a1 = pa[y - 1], a2 = pa[y - 2], a3 = pa[y - 3];
-          if (a0 == q) { hit = y; break; }
-          if (a1 == q) { hit = y - 1; break; }
-          if (a2 == q) { hit = y - 2; break; }
-          if (a3 == q) { hit = y - 3; break; }
-          y -= 4;
+        // the latest entry at q among [0, tid): aligned groups of 16, the
+        // first one cut at tid - 1
+        const int4* pa4 = reinterpret_cast<const int4*>(cpa[b]);
+        int hit = -1;
+        for (int g0 = (tid - 1) & ~15; g0 >= 0; g0 -= 16) {
+          int4 v[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = pa4[g0 / 4 + k];
+          uint32_t m = 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            m |= ((uint32_t)(v[k].x == q) | (uint32_t)(v[k].y == q) << 1 | (uint32_t)(v[k].z == q) << 2 |
+                  (uint32_t)(v[k].w == q) << 3)
+                 << (4 * k);
+          const int lim = tid - 1 - g0;  // entries g0 + [0, lim] lie before this row
+          if (lim < 15) m &= (2u << lim) - 1u;
+          if (m) {
+            hit = g0 + 31 - __clz((int)m);
+            break;
+          }
         }
-        if (hit < 0)
-          for (; y >= 0; --y)
-            if (pa[y] == q) {
-              hit = y;
-              break;
-            }
         const bool past = (int64_t)f < thr;
         if (hit >= 0) {
           if (cfr[b][hit] < f) {
