@@ -127,12 +127,12 @@ def oracle_mode(mode: int) -> int:
     return sum(o for g, o in pairs if mode & g)
 
 
-def check_pass(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, got: GpuPass):
+def check_pass(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, got: GpuPass, cv_tau=None):
     """Every rule above for one pass in any mode; K, V, fr, pa are the cache
     before the pass. Returns the near-threshold row count."""
     om = oracle_mode(mode)
     tar64 = oracle.tar_scores(K, fr, pa, n, r, gh, gw, mode=om)
-    van64, _ = oracle.van_scores(V, fr, pa, n, gh, gw)
+    van64, _ = oracle.van_scores(V, fr, pa, n, gh, gw, cv_tau)
     sel = oracle.select(tar64.astype(np.float32), van64.astype(np.float32), fr, n, budget, alpha, r, mode=om)
     check_scores(got.tar, got.van, tar64, van64, n, name)
     check_ascending(got.keep, n)

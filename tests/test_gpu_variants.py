@@ -14,7 +14,7 @@ from tests.test_gpu_parity import cache_of
 pytestmark = pytest.mark.gpu
 
 
-def gpu_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps=False):
+def gpu_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps=False, cv_tau=None):
     kind = "bf16" if K.dtype == np.uint16 else "raw"
     Kd, Vd, frd, pad = P.to_device(K, kind), P.to_device(V, kind), P.to_device(fr), P.to_device(pa)
     B, L, H, S, D = K.shape
@@ -29,17 +29,17 @@ def gpu_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps=False):
         ipv.ipv_select(tar, van, frd, n, budget, alpha, r, keep, ws, gh, gw, head_dim=D, dtype=shape.dtype, mode=mode)
         ipv.ipv_compact(Kd, Vd, frd, pad, n, keep, budget, ws, gh, gw)
     else:
-        ipv.ipv_compress(Kd, Vd, frd, pad, n, budget, alpha, r, None, tar, van, keep, ws, gh, gw, mode=mode)
+        ipv.ipv_compress(Kd, Vd, frd, pad, n, budget, alpha, r, cv_tau, tar, van, keep, ws, gh, gw, mode=mode)
     torch.cuda.synchronize()
     return P.GpuPass(P.to_host(tar), P.to_host(van), P.to_host(keep), P.to_host(Kd), P.to_host(Vd), P.to_host(frd),
                      P.to_host(pad), ipv.ipv_read_device_errors(ws))
 
 
-def mode_check(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps=False):
+def mode_check(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps=False, cv_tau=None):
     print("case %s mode=%d alpha=%s n=%d C=%d steps=%s" % (name, mode, alpha, n, budget, steps), flush=True)
-    got = gpu_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps)
+    got = gpu_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, steps, cv_tau)
     assert got.errors == 0
-    near = P.check_pass(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, got)
+    near = P.check_pass(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, got, cv_tau)
     print("  near-threshold rows %d" % near, flush=True)
     return got
 
@@ -59,6 +59,14 @@ def test_7b_class_modes_through_the_step_entry_points(mode):
     w = W.SEVEN_B
     mode_check(w.name, *cache_of(w), w.n_tokens, w.budget, 0.5, w.recent_frames, w.grid_h, w.grid_w, mode,
                steps=True)
+
+
+@pytest.mark.parametrize("mode", [ipv.TAR_ADJACENT, ipv.HEAD_SHARED | ipv.VAN_REVERSE])
+def test_modes_with_layer_adaptive_pooling(mode):
+    # VaN is pooled after the sweep (with consecutive-frame TaR: after the adjacent sweep that computes it)
+    w = W.POOL
+    mode_check(w.name, *cache_of(w), w.n_tokens, w.budget, 0.5, w.recent_frames, w.grid_h, w.grid_w, mode,
+               cv_tau=w.cv_tau)
 
 
 @pytest.mark.parametrize("alpha", [1.0, 0.0])
