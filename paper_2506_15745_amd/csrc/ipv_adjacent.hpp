@@ -4,7 +4,7 @@
 // contrasts TaR variants). Score -cos(K[x], K[prev(x)]), 0 with no such row.
 //
 // Two kernels:
-//   k_prev_rows       one 1024-thread block per slice walks the rows in chunks
+//   k_prev_rows       one 1024-thread block per slice takes the rows in chunks
 //                     of 1024 and writes prev(x) (or -1) for every valid row;
 //                     it also publishes the slice's first recent row and,
 //                     optionally, zeroes the slice's compaction flags.
@@ -21,19 +21,19 @@ constexpr int kPrevThreads = 1024;
 constexpr int kPrevMaxPositions = 8192;
 
 // prev(x), with frame ids non-decreasing along the rows: the latest row y < x
-// at x's patch position whose frame is older than x's. Inside a chunk a row
-// walks back over the chunk's own metadata (in LDS); if its position does not
-// occur earlier in the chunk, `last[q]` (the latest row at q in the chunks
-// before) is the answer. A second row with the same (frame, patch) pair, or a
-// frame id that decreases, or a patch id outside [0, p), sets an error bit;
-// such metadata gives no defined prev.
+// at x's patch position whose frame is older than x's. The rows are taken in
+// chunks of 1024, one row per thread. Inside a chunk the rows are bucketed by
+// position with a counting sort in LDS (an atomic rank per row, an exclusive
+// scan over the p counters, a scatter), so a row finds the latest earlier row
+// of its position in the same chunk by looking through its own bucket only
+// (about 1024 / p entries); if there is none, `last[q]` (the latest row at q
+// in the chunks before) is the answer, and the row that is the last of its
+// bucket updates `last[q]` for the next chunk. A second row with the same
+// (frame, patch) pair, a frame id that decreases, or a patch id outside
+// [0, p) sets an error bit; such metadata gives no defined prev.
 //
-// A walk reads 16 patch ids per step with four aligned 16-byte LDS reads and
-// tests them all before it branches, so a step costs one LDS round trip.
-//
-// The chunk metadata is double-buffered, so one chunk costs two barriers:
-// (A) the chunk's metadata is visible, (B) every walk has read `last` and the
-// carry; then `last` and the carry are updated for the next chunk.
+// The chunk metadata is double-buffered; a chunk costs six barriers and no
+// global-memory round trip (the next chunk's loads are in flight meanwhile).
 __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __restrict__ frame_idx,
                                                             const int32_t* __restrict__ patch_idx, int64_t S,
                                                             int32_t n, int32_t r, int32_t p,
@@ -41,9 +41,12 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
                                                             int32_t* __restrict__ first_recent, uint32_t* err,
                                                             uint32_t* __restrict__ zero, int32_t zero_per_slice) {
   constexpr int NT = kPrevThreads;
+  constexpr int BPT = (kPrevMaxPositions + 1 + NT - 1) / NT;  // scan entries per thread
   __shared__ int32_t last[kPrevMaxPositions];
-  __shared__ alignas(16) int32_t cpa[2][NT];
-  __shared__ int32_t cfr[2][NT];
+  __shared__ int32_t cnt[kPrevMaxPositions + 1];  // counts, then bucket starts (cnt[p] = rows bucketed)
+  __shared__ int32_t bucket[NT];
+  __shared__ int32_t cpa[2][NT], cfr[2][NT];
+  __shared__ int32_t scan_tot[NT / kWave];
   // carry: frame id of the previous chunk's last row, and the row its frame starts at
   __shared__ int32_t carry_frame, carry_start;
   const int tid = threadIdx.x;
@@ -52,6 +55,7 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
   if (zero)
     for (int i = tid; i < zero_per_slice; i += NT) zero[slice * zero_per_slice + i] = 0u;
   for (int q = tid; q < p; q += NT) last[q] = -1;
+  for (int q = tid; q <= p; q += NT) cnt[q] = 0;
   if (tid == 0) {
     carry_frame = INT32_MIN;
     carry_start = 0;
@@ -65,44 +69,55 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
     const int64_t x = c0 + tid;
     const bool valid = x < n;
     const int32_t f = nf, q = np;
+    const bool inq = valid && q >= 0 && q < p;
     cpa[b][tid] = q;
     cfr[b][tid] = f;
-    __syncthreads();  // (A)
-    {  // the next chunk's metadata is on its way during the walks
+    __syncthreads();  // (A) chunk metadata visible; counters zero
+    {  // the next chunk's metadata is on its way meanwhile
       const int64_t xn = min(c0 + NT + tid, (int64_t)n - 1);
       nf = frame_idx[base + xn];
       np = patch_idx[base + xn];
     }
+    const int32_t rank = inq ? atomicAdd(&cnt[q], 1) : 0;
+    __syncthreads();  // (B) counts complete
+    {  // exclusive scan of cnt[0..p] in place: thread t owns entries [t*BPT, (t+1)*BPT)
+      int32_t v[BPT], sum = 0;
+#pragma unroll
+      for (int i = 0; i < BPT; ++i) {
+        const int e = tid * BPT + i;
+        v[i] = e <= p ? cnt[e] : 0;
+        sum += v[i];
+      }
+      int32_t total;
+      int32_t run = block_exclusive_scan<NT>(sum, scan_tot, &total);
+#pragma unroll
+      for (int i = 0; i < BPT; ++i) {
+        const int e = tid * BPT + i;
+        if (e <= p) cnt[e] = run;
+        run += v[i];
+      }
+    }
+    __syncthreads();  // (C) bucket starts visible
+    if (inq) bucket[cnt[q] + rank] = tid;
+    __syncthreads();  // (D) buckets filled
     const int32_t cf = carry_frame, cs = carry_start;
-    const int cnt = (int)min((int64_t)NT, (int64_t)n - c0);
+    const int cnt_rows = (int)min((int64_t)NT, (int64_t)n - c0);
     int32_t pred = -1;
+    bool last_of_bucket = true;
     if (valid) {
       const int32_t fprev = tid > 0 ? cfr[b][tid - 1] : cf;
       if (f < fprev) ebits |= 2u;
       if ((int64_t)f >= thr && (int64_t)fprev < thr) first_recent[slice] = (int32_t)x;
-      if (q < 0 || q >= p) {
+      if (!inq) {
         ebits |= 1u;
       } else {
-        // the latest entry at q among [0, tid): aligned groups of 16, the
-        // first one cut at tid - 1
-        const int4* pa4 = reinterpret_cast<const int4*>(cpa[b]);
+        // the latest row of this chunk before x at position q
         int hit = -1;
-        for (int g0 = (tid - 1) & ~15; g0 >= 0; g0 -= 16) {
-          int4 v[4];
-#pragma unroll
-          for (int k = 0; k < 4; ++k) v[k] = pa4[g0 / 4 + k];
-          uint32_t m = 0;
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            m |= ((uint32_t)(v[k].x == q) | (uint32_t)(v[k].y == q) << 1 | (uint32_t)(v[k].z == q) << 2 |
-                  (uint32_t)(v[k].w == q) << 3)
-                 << (4 * k);
-          const int lim = tid - 1 - g0;  // entries g0 + [0, lim] lie before this row
-          if (lim < 15) m &= (2u << lim) - 1u;
-          if (m) {
-            hit = g0 + 31 - __clz((int)m);
-            break;
-          }
+        const int lo = cnt[q], hi = cnt[q + 1];
+        for (int i = lo; i < hi; ++i) {
+          const int e = bucket[i];
+          if (e < tid) hit = max(hit, e);
+          last_of_bucket &= e <= tid;
         }
         const bool past = (int64_t)f < thr;
         if (hit >= 0) {
@@ -119,10 +134,11 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
       }
       prev[base + x] = pred;
     }
-    __syncthreads();  // (B)
-    if (valid && q >= 0 && q < p) atomicMax(&last[q], (int32_t)x);
-    const int32_t fl = cfr[b][cnt - 1];
-    if (tid == cnt - 1) carry_frame = fl;
+    __syncthreads();  // (E) every row has read last[], the buckets and the carry
+    if (inq && last_of_bucket) last[q] = (int32_t)x;
+    for (int e = tid; e <= p; e += NT) cnt[e] = 0;
+    const int32_t fl = cfr[b][cnt_rows - 1];
+    if (tid == cnt_rows - 1) carry_frame = fl;
     // the row where the last row's frame starts, if it starts in this chunk
     if (valid && f == fl && (tid > 0 ? cfr[b][tid - 1] != fl : cf != fl)) carry_start = (int32_t)x;
   }

@@ -131,6 +131,26 @@ __device__ __forceinline__ void wave_min_max(uint32_t& mn, uint32_t& mx) {
   mx = b;
 }
 
+// Exclusive prefix sum over the workgroup in thread order (one barrier);
+// *total gets the sum. `tot` is used by this scan only.
+template <int NT>
+__device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t* tot, int32_t* total) {
+  constexpr int NW = NT / kWave;
+  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+  const int32_t incl = wave_inclusive_scan(v);
+  if (lane == kWave - 1) tot[w] = incl;
+  __syncthreads();
+  int32_t off = 0, sum = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const int32_t t = tot[i];
+    off += i < w ? t : 0;
+    sum += t;
+  }
+  *total = sum;
+  return incl - v + off;
+}
+
 __device__ inline void raise_error(uint32_t* err, uint32_t bits) {
   if (err) atomicOr(err, bits);
 }
