@@ -24,8 +24,11 @@
  *
  * ---------------------------------------------------------------- layouts
  * A cache holds B streams x L layers x H KV heads; each (b, l, h) "slice" has
- * a row capacity S of which rows [0, n) are valid (n = n_tokens, the same for
- * every slice of a call). All row-major:
+ * a row capacity S of which rows [0, n_tokens[b]) are valid. n_tokens is a
+ * HOST array of B row counts (streams fill at their own pace); a stream with
+ * 0 rows is left alone by every call except ipv_append. The work is launched
+ * once per maximal run of consecutive streams with the same count, so a batch
+ * at one fill level is one launch per kernel. All row-major:
  *   K, V        [B, L, H, S, D] elements of `dtype` (bf16 or fp32), device
  *   frame_idx   [B, L, H, S] int32, device: frame id of each row
  *   patch_idx   [B, L, H, S] int32, device: patch position in [0, grid_h*grid_w)
@@ -76,7 +79,7 @@ typedef enum {
   IPV_OK = 0,
   IPV_ERR_NULL = 1,        /* a required pointer is NULL */
   IPV_ERR_ALIGN = 2,       /* a pointer breaks the alignment rules above */
-  IPV_ERR_SHAPE = 3,       /* bad B/L/H/D/S/grid, n outside [1, S], or a size the kernels do not cover */
+  IPV_ERR_SHAPE = 3,       /* bad B/L/H/D/S/grid, a row count outside [0, S], or a size the kernels do not cover */
   IPV_ERR_DTYPE = 4,       /* dtype is neither IPV_BF16 nor IPV_F32 */
   IPV_ERR_BUDGET = 5,      /* budget outside [min(n, r*p), n] */
   IPV_ERR_ARG = 6,         /* alpha outside [0, 1], recent_frames < 1, bad cv_tau */
@@ -143,7 +146,7 @@ ipv_status ipv_workspace_bytes(const ipv_shape* shape, size_t* bytes);
  * mode & IPV_TAR_ADJACENT: the consecutive-frame score described at that bit.
  */
 ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* frame_idx,
-                          const int32_t* patch_idx, int32_t n_tokens, int32_t recent_frames, uint32_t mode,
+                          const int32_t* patch_idx, const int32_t* n_tokens, int32_t recent_frames, uint32_t mode,
                           float* tar, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -157,7 +160,7 @@ ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* 
  * cv_tau NULL: no pooling. pool_size (device, [B, L], may be NULL) receives k.
  */
 ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* frame_idx,
-                          const int32_t* patch_idx, int32_t n_tokens, const double* cv_tau, float* van,
+                          const int32_t* patch_idx, const int32_t* n_tokens, const double* cv_tau, float* van,
                           int32_t* pool_size, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -171,26 +174,27 @@ ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* 
  * still to the lower row index); IPV_HEAD_SHARED selects once per layer.
  */
 ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van, const int32_t* frame_idx,
-                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                      const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
                       int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * In-place compaction (Sec. 3.1; Algorithm 1 step (5)): for j < C, row j of
  * K, V, frame_idx and patch_idx becomes a bit copy of row keep_idx[j]. Needs
  * keep_idx[j] in [j, n) (true for any ascending keep set); rows [C, S) are
- * left unspecified and free for new frames. The caller then sets n = C.
+ * left unspecified and free for new frames. The caller then sets n_tokens[b] = C
+ * for every stream with n_tokens[b] > 0.
  * All chunks of all slices are copied in parallel; a chunk stores only after
  * every earlier chunk that reads its rows has loaded them (flags in ws).
  */
 ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                       int32_t n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
+                       const int32_t* n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
                        void* stream);
 
 /* The whole pass: ipv_tar_scores, ipv_van_scores, ipv_select, ipv_compact,
    each with the same mode (with IPV_TAR_ADJACENT the VaN scores are computed
    in the same sweep as the consecutive-frame TaR scores). */
 ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                        const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
                         const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
                         size_t ws_bytes, void* stream);
 
@@ -201,45 +205,48 @@ ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame
  *   (IPV_TAR_ADJACENT: before the prev-row walk, before the adjacent sweep)
  *   at[2] before pooling                at[3] before selection
  *   at[4] before compaction             at[5] after compaction
- * Elapsed time between consecutive events is that step's device time.
+ * Elapsed time between consecutive events is that step's device time. With
+ * several runs of equal row counts the events are recorded in each run, so
+ * they end up timing the last run.
  */
 typedef struct {
   void* at[6];
 } ipv_events;
 
 ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                              int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                              const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames,
                               uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx,
                               void* ws, size_t ws_bytes, void* stream, const ipv_events* events);
 
 /*
  * Append new rows to every slice (Algorithm 1 step (1): the tokens of a new
  * frame, or part of one, join the cache after prefill). Rows
- * [n_tokens, n_tokens + rows) of each slice receive K_new / V_new
+ * [n_tokens[b], n_tokens[b] + rows) of each slice of stream b receive K_new / V_new
  * ([B, L, H, rows, D], same dtype as the cache, device, 16-byte aligned),
  * frame_idx = frame_id and patch_idx = first_patch + i for the i-th new row.
- * Needs n_tokens >= 0, rows >= 1, n_tokens + rows <= S and
- * first_patch + rows <= p. The caller's row count becomes n_tokens + rows.
+ * Needs n_tokens[b] >= 0, rows >= 1, n_tokens[b] + rows <= S and
+ * first_patch + rows <= p. Stream b's row count becomes n_tokens[b] + rows.
  */
 ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                      int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                      const int32_t* n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
                       int32_t first_patch, void* stream);
 
 /*
  * One iteration of continual KV cache compression (Algorithm 1; Sec. 3):
- * append the new rows (ipv_append), and if the cache then holds
- * len >= mem_cap rows, compress it to `budget` rows (ipv_compress with the
- * given alpha, recent_frames, mode and cv_tau). *n_out (host) receives the row
- * count after the step and *compressed (host) whether the pass ran.
- * Needs budget <= mem_cap <= S and n_tokens < mem_cap (the previous step
- * left the cache below the cap). Positions: the cache holds keys before the
+ * append the new rows to every stream (ipv_append), and compress to `budget`
+ * rows every stream that then holds len >= mem_cap rows (ipv_compress with
+ * the given alpha, recent_frames, mode and cv_tau; the other streams are left
+ * alone). n_out[b] and compressed[b] (host arrays of B) receive each stream's
+ * row count after the step and whether its pass ran.
+ * Needs budget <= mem_cap <= S and n_tokens[b] < mem_cap (the previous step
+ * left every stream below the cap). Positions: the cache holds keys before the
  * rotary position encoding and compaction keeps the order of the kept rows,
  * so after every step row j takes position j at decoding, which stays below
  * mem_cap + rows (appendix, positional-encoding details); no position array
  * is stored.
  */
 ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                        int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                        const int32_t* n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
                         int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
                         uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
                         int32_t* n_out, int32_t* compressed, void* stream);

@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <vector>
 
 #include "../../include/ipv.h"
 #include "ipv_adjacent.hpp"
@@ -313,6 +314,85 @@ ipv_status check_tau(const double* tau) {
   return IPV_OK;
 }
 
+// ------------------------------------------------------------ per-stream row counts
+// Every call takes n_tokens as a host array of B row counts. The work is
+// launched once per maximal run of consecutive streams with the same count
+// (one run for a batch at one fill level); a stream with 0 rows is left alone.
+// A run is a contiguous sub-batch: the same layouts with fewer streams, so the
+// kernels see one count, and the runs reuse the workspace one after another
+// on the stream.
+Dims sub_batch(const Dims& d, int64_t nb) {
+  Dims s = d;
+  s.B = nb;
+  s.slices = nb * d.L * d.H;
+  return s;
+}
+
+template <typename T>
+T* at_stream(T* p, int64_t b0, int64_t per_stream_elems) {
+  return p ? p + b0 * per_stream_elems : p;
+}
+
+// fn(sub-batch dims, first stream, row count) for every run with a non-zero count
+template <typename F>
+ipv_status for_each_run(const Dims& d, const int32_t* n_tokens, F fn) {
+  for (int64_t b = 0; b < d.B;) {
+    const int32_t n = n_tokens[b];
+    int64_t e = b + 1;
+    while (e < d.B && n_tokens[e] == n) ++e;
+    if (n > 0) IPV_TRY(fn(sub_batch(d, e - b), b, n));
+    b = e;
+  }
+  return IPV_OK;
+}
+
+// every count in [0, min(S, kMaxRows)]; `each` checks the non-zero ones further
+template <typename F>
+ipv_status check_counts(const Dims& d, const int32_t* n_tokens, F each) {
+  if (!n_tokens) return IPV_ERR_NULL;
+  for (int64_t b = 0; b < d.B; ++b) {
+    const int32_t n = n_tokens[b];
+    if (n < 0 || n > d.S || n > kMaxRows) return IPV_ERR_SHAPE;
+    if (n > 0) IPV_TRY(each(n));
+  }
+  return IPV_OK;
+}
+
+ipv_status no_check(int32_t) { return IPV_OK; }
+
+ipv_status check_pass_args(const Dims& d, const int32_t* n_tokens, int32_t budget, double alpha, int32_t r,
+                           const double* cv_tau, uint32_t mode) {
+  IPV_TRY(check_recent(d, r));
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
+  IPV_TRY(check_counts(d, n_tokens, [&](int32_t n) { return check_budget(d, n, budget, r); }));
+  IPV_TRY(check_tau(cv_tau));
+  return check_mode(mode);
+}
+
+// the whole pass on one run; events (may be NULL) as in ipv_compress_timed
+ipv_status compress_run(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, int32_t budget,
+                        double alpha, int32_t r, uint32_t mode, const double* cv_tau, float* tar, float* van,
+                        int32_t* keep, void* ws, hipStream_t st, const ipv_events* events) {
+  auto mark = [&](int i) -> ipv_status {
+    if (!events || !events->at[i]) return IPV_OK;
+    return hipEventRecord(static_cast<hipEvent_t>(events->at[i]), st) == hipSuccess ? IPV_OK : IPV_ERR_HIP;
+  };
+  IPV_TRY(mark(0));
+  IPV_TRY(scores(d, K, V, fr, pa, n, r, tar, van, ws, st, [&]() { return mark(1); }, compact_chunks(budget),
+                 (mode & IPV_TAR_ADJACENT) != 0));
+  IPV_TRY(mark(2));
+  if (cv_tau) IPV_TRY(pool_d(d, cv_tau, van, fr, pa, n, nullptr, ws, st));
+  IPV_TRY(mark(3));
+  IPV_TRY(select(d, tar, van, fr, n, budget, floor_share(alpha, budget), r, keep, err_word(ws), st, mode));
+  IPV_TRY(mark(4));
+  IPV_TRY(compact(d, K, V, fr, pa, n, keep, budget, ws, st, true));
+  return mark(5);
+}
+
+// per-stream element counts of the arrays
+int64_t kv_bytes_per_stream(const Dims& d) { return d.L * d.H * d.S * d.D * d.elem; }
+int64_t rows_per_stream(const Dims& d) { return d.L * d.H * d.S; }
+
 }  // namespace
 
 extern "C" {
@@ -326,61 +406,71 @@ ipv_status ipv_workspace_bytes(const ipv_shape* shape, size_t* bytes) {
 }
 
 ipv_status ipv_tar_scores(const ipv_shape* shape, const void* K, const int32_t* frame_idx, const int32_t* patch_idx,
-                          int32_t n_tokens, int32_t recent_frames, uint32_t mode, float* tar, void* ws,
+                          const int32_t* n_tokens, int32_t recent_frames, uint32_t mode, float* tar, void* ws,
                           size_t ws_bytes, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
   if (!K || !frame_idx || !patch_idx || !tar) return IPV_ERR_NULL;
   if (!aligned(K, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) || !aligned(tar, 16)) return IPV_ERR_ALIGN;
-  IPV_TRY(check_rows(d, n_tokens));
+  IPV_TRY(check_counts(d, n_tokens, no_check));
   IPV_TRY(check_recent(d, recent_frames));
   IPV_TRY(check_mode(mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
-  return scores(d, K, nullptr, frame_idx, patch_idx, n_tokens, recent_frames, tar, nullptr, ws,
-                static_cast<hipStream_t>(stream), no_mark, 0, (mode & IPV_TAR_ADJACENT) != 0);
+  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d);
+  return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {
+    return scores(s, static_cast<const char*>(K) + b0 * kb, nullptr, frame_idx + b0 * rs, patch_idx + b0 * rs, n,
+                  recent_frames, tar + b0 * rs, nullptr, ws, static_cast<hipStream_t>(stream), no_mark, 0,
+                  (mode & IPV_TAR_ADJACENT) != 0);
+  });
 }
 
 ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* frame_idx, const int32_t* patch_idx,
-                          int32_t n_tokens, const double* cv_tau, float* van, int32_t* pool_size, void* ws,
+                          const int32_t* n_tokens, const double* cv_tau, float* van, int32_t* pool_size, void* ws,
                           size_t ws_bytes, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
   if (!V || !frame_idx || !patch_idx || !van) return IPV_ERR_NULL;
   if (!aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) || !aligned(van, 16)) return IPV_ERR_ALIGN;
   if (pool_size && !aligned(pool_size, 4)) return IPV_ERR_ALIGN;
-  IPV_TRY(check_rows(d, n_tokens));
+  IPV_TRY(check_counts(d, n_tokens, no_check));
   IPV_TRY(check_tau(cv_tau));
   IPV_TRY(check_ws(d, ws, ws_bytes));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  IPV_TRY(scores(d, nullptr, V, frame_idx, patch_idx, n_tokens, 1, nullptr, van, ws, st));
-  if (cv_tau) return pool_d(d, cv_tau, van, frame_idx, patch_idx, n_tokens, pool_size, ws, st);
-  if (pool_size) {
-    const int64_t cnt = d.B * d.L;
-    k_fill_i32<<<dim3((uint32_t)((cnt + 255) / 256)), dim3(256), 0, st>>>(pool_size, cnt, 1);
-    return launched();
-  }
-  return IPV_OK;
+  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d);
+  return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) -> ipv_status {
+    const int32_t* fr = frame_idx + b0 * rs;
+    const int32_t* pa = patch_idx + b0 * rs;
+    float* vn = van + b0 * rs;
+    int32_t* ps = at_stream(pool_size, b0, d.L);
+    IPV_TRY(scores(s, nullptr, static_cast<const char*>(V) + b0 * kb, fr, pa, n, 1, nullptr, vn, ws, st));
+    if (cv_tau) return pool_d(s, cv_tau, vn, fr, pa, n, ps, ws, st);
+    if (ps) {
+      const int64_t cnt = s.B * s.L;
+      k_fill_i32<<<dim3((uint32_t)((cnt + 255) / 256)), dim3(256), 0, st>>>(ps, cnt, 1);
+      return launched();
+    }
+    return IPV_OK;
+  });
 }
 
 ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van, const int32_t* frame_idx,
-                      int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                      const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
                       int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
   if (!tar || !van || !frame_idx || !keep_idx) return IPV_ERR_NULL;
   if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(frame_idx, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
-  IPV_TRY(check_rows(d, n_tokens));
-  IPV_TRY(check_recent(d, recent_frames));
-  if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
-  IPV_TRY(check_budget(d, n_tokens, budget, recent_frames));
-  IPV_TRY(check_mode(mode));
+  IPV_TRY(check_pass_args(d, n_tokens, budget, alpha, recent_frames, nullptr, mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
-  return select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
-                err_word(ws), static_cast<hipStream_t>(stream), mode);
+  const int64_t rs = rows_per_stream(d), ks = d.L * d.H * (int64_t)budget;
+  return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {
+    return select(s, tar + b0 * rs, van + b0 * rs, frame_idx + b0 * rs, n, budget, floor_share(alpha, budget),
+                  recent_frames, keep_idx + b0 * ks, err_word(ws), static_cast<hipStream_t>(stream), mode);
+  });
 }
 
 ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                       int32_t n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
+                       const int32_t* n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
                        void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
@@ -388,49 +478,37 @@ ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
       !aligned(keep_idx, 16))
     return IPV_ERR_ALIGN;
-  IPV_TRY(check_rows(d, n_tokens));
-  if (budget < 1 || budget > n_tokens) return IPV_ERR_BUDGET;
+  IPV_TRY(check_counts(d, n_tokens, [&](int32_t n) { return budget < 1 || budget > n ? IPV_ERR_BUDGET : IPV_OK; }));
   IPV_TRY(check_ws(d, ws, ws_bytes));
-  return compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, static_cast<hipStream_t>(stream));
+  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), ks = d.L * d.H * (int64_t)budget;
+  return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {
+    return compact(s, static_cast<char*>(K) + b0 * kb, static_cast<char*>(V) + b0 * kb, frame_idx + b0 * rs,
+                   patch_idx + b0 * rs, n, keep_idx + b0 * ks, budget, ws, static_cast<hipStream_t>(stream));
+  });
 }
 
 ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                              int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
-                              const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
-                              size_t ws_bytes, void* stream, const ipv_events* events) {
+                              const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                              uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx,
+                              void* ws, size_t ws_bytes, void* stream, const ipv_events* events) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
   if (!K || !V || !frame_idx || !patch_idx || !tar || !van || !keep_idx) return IPV_ERR_NULL;
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
       !aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16))
     return IPV_ERR_ALIGN;
-  IPV_TRY(check_rows(d, n_tokens));
-  IPV_TRY(check_recent(d, recent_frames));
-  if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
-  IPV_TRY(check_budget(d, n_tokens, budget, recent_frames));
-  IPV_TRY(check_tau(cv_tau));
-  IPV_TRY(check_mode(mode));
+  IPV_TRY(check_pass_args(d, n_tokens, budget, alpha, recent_frames, cv_tau, mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  auto mark = [&](int i) -> ipv_status {
-    if (!events || !events->at[i]) return IPV_OK;
-    return hipEventRecord(static_cast<hipEvent_t>(events->at[i]), st) == hipSuccess ? IPV_OK : IPV_ERR_HIP;
-  };
-  IPV_TRY(mark(0));
-  IPV_TRY(scores(d, K, V, frame_idx, patch_idx, n_tokens, recent_frames, tar, van, ws, st,
-                 [&]() { return mark(1); }, compact_chunks(budget), (mode & IPV_TAR_ADJACENT) != 0));
-  IPV_TRY(mark(2));
-  if (cv_tau) IPV_TRY(pool_d(d, cv_tau, van, frame_idx, patch_idx, n_tokens, nullptr, ws, st));
-  IPV_TRY(mark(3));
-  IPV_TRY(select(d, tar, van, frame_idx, n_tokens, budget, floor_share(alpha, budget), recent_frames, keep_idx,
-                 err_word(ws), st, mode));
-  IPV_TRY(mark(4));
-  IPV_TRY(compact(d, K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, st, true));
-  return mark(5);
+  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), ks = d.L * d.H * (int64_t)budget;
+  return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {
+    return compress_run(s, static_cast<char*>(K) + b0 * kb, static_cast<char*>(V) + b0 * kb, frame_idx + b0 * rs,
+                        patch_idx + b0 * rs, n, budget, alpha, recent_frames, mode, cv_tau, tar + b0 * rs,
+                        van + b0 * rs, keep_idx + b0 * ks, ws, static_cast<hipStream_t>(stream), events);
+  });
 }
 
 ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                        int32_t n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
+                        const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames, uint32_t mode,
                         const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
                         void* stream) {
   return ipv_compress_timed(shape, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, mode, cv_tau,
@@ -438,56 +516,72 @@ ipv_status ipv_compress(const ipv_shape* shape, void* K, void* V, int32_t* frame
 }
 
 ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                      int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                      const int32_t* n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
                       int32_t first_patch, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
-  if (!K || !V || !frame_idx || !patch_idx || !K_new || !V_new) return IPV_ERR_NULL;
+  if (!K || !V || !frame_idx || !patch_idx || !K_new || !V_new || !n_tokens) return IPV_ERR_NULL;
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
       !aligned(K_new, 16) || !aligned(V_new, 16))
     return IPV_ERR_ALIGN;
-  if (n_tokens < 0 || rows < 1 || (int64_t)n_tokens + rows > d.S) return IPV_ERR_SHAPE;
+  if (rows < 1) return IPV_ERR_SHAPE;
+  for (int64_t b = 0; b < d.B; ++b)
+    if (n_tokens[b] < 0 || (int64_t)n_tokens[b] + rows > d.S) return IPV_ERR_SHAPE;
   if (first_patch < 0 || (int64_t)first_patch + rows > d.p) return IPV_ERR_ARG;
   const int64_t RB = d.D * d.elem;
-  const int64_t chunks = d.slices * rows * (RB / 16);
-  const uint32_t blocks = (uint32_t)std::min<int64_t>((chunks + 255) / 256, 65536);
-  k_append<<<dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream)>>>(
-      static_cast<const char*>(K_new), static_cast<const char*>(V_new), static_cast<char*>(K), static_cast<char*>(V),
-      frame_idx, patch_idx, d.S, n_tokens, rows, RB, frame_id, first_patch, d.slices);
-  return launched();
+  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), nb = d.L * d.H * (int64_t)rows * RB;
+  // runs of equal counts; an empty stream appends at row 0 like any other
+  for (int64_t b = 0; b < d.B;) {
+    const int32_t n = n_tokens[b];
+    int64_t e = b + 1;
+    while (e < d.B && n_tokens[e] == n) ++e;
+    const int64_t slices = (e - b) * d.L * d.H;
+    const int64_t chunks = slices * rows * (RB / 16);
+    const uint32_t blocks = (uint32_t)std::min<int64_t>((chunks + 255) / 256, 65536);
+    k_append<<<dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream)>>>(
+        static_cast<const char*>(K_new) + b * nb, static_cast<const char*>(V_new) + b * nb,
+        static_cast<char*>(K) + b * kb, static_cast<char*>(V) + b * kb, frame_idx + b * rs, patch_idx + b * rs, d.S,
+        n, rows, RB, frame_id, first_patch, slices);
+    IPV_TRY(launched());
+    b = e;
+  }
+  return IPV_OK;
 }
 
 ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
-                        int32_t n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
+                        const int32_t* n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frame_id,
                         int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
-                        uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
-                        int32_t* n_out, int32_t* compressed, void* stream) {
+                        uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws,
+                        size_t ws_bytes, int32_t* n_out, int32_t* compressed, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
-  if (!n_out || !compressed) return IPV_ERR_NULL;
-  if (mem_cap < 1 || mem_cap > d.S || n_tokens >= mem_cap) return IPV_ERR_SHAPE;
+  if (!n_out || !compressed || !n_tokens) return IPV_ERR_NULL;
+  if (mem_cap < 1 || mem_cap > d.S) return IPV_ERR_SHAPE;
   if (budget > mem_cap) return IPV_ERR_BUDGET;
-  const int32_t n1 = n_tokens + rows;
-  if (n1 >= mem_cap) {
+  // the row counts after the append; the streams that reach the cap run the pass
+  std::vector<int32_t> after((size_t)d.B), pass((size_t)d.B);
+  bool any = false;
+  for (int64_t b = 0; b < d.B; ++b) {
+    if (n_tokens[b] < 0 || n_tokens[b] >= mem_cap) return IPV_ERR_SHAPE;
+    after[b] = n_tokens[b] + rows;
+    pass[b] = after[b] >= mem_cap ? after[b] : 0;
+    any |= pass[b] > 0;
+  }
+  if (any) {
     // every argument of the pass is checked before the append is enqueued
-    if (!tar || !van || !keep_idx) return IPV_ERR_NULL;
+    if (!tar || !van || !keep_idx || !K || !V || !frame_idx || !patch_idx) return IPV_ERR_NULL;
     if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
-    IPV_TRY(check_rows(d, n1));
-    IPV_TRY(check_recent(d, recent_frames));
-    if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
-    IPV_TRY(check_budget(d, n1, budget, recent_frames));
-    IPV_TRY(check_tau(cv_tau));
-    IPV_TRY(check_mode(mode));
+    IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode));
     IPV_TRY(check_ws(d, ws, ws_bytes));
   }
   IPV_TRY(ipv_append(shape, K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, rows, frame_id, first_patch, stream));
-  *n_out = n1;
-  *compressed = 0;
-  if (n1 < mem_cap) return IPV_OK;
-  IPV_TRY(ipv_compress(shape, K, V, frame_idx, patch_idx, n1, budget, alpha, recent_frames, mode, cv_tau, tar, van,
-                       keep_idx, ws, ws_bytes, stream));
-  *n_out = budget;
-  *compressed = 1;
+  if (any)
+    IPV_TRY(ipv_compress(shape, K, V, frame_idx, patch_idx, pass.data(), budget, alpha, recent_frames, mode, cv_tau,
+                         tar, van, keep_idx, ws, ws_bytes, stream));
+  for (int64_t b = 0; b < d.B; ++b) {
+    n_out[b] = pass[b] > 0 ? budget : after[b];
+    compressed[b] = pass[b] > 0;
+  }
   return IPV_OK;
 }
 

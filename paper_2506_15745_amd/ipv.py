@@ -70,16 +70,17 @@ def lib() -> ctypes.CDLL:
         sp = ctypes.POINTER(Shape)
         L.ipv_workspace_bytes.argtypes = [sp, ctypes.POINTER(ctypes.c_size_t)]
         u32 = ctypes.c_uint32
-        L.ipv_tar_scores.argtypes = [sp, vp, vp, vp, i32, i32, u32, vp, vp, sz, vp]
-        L.ipv_van_scores.argtypes = [sp, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
-        L.ipv_select.argtypes = [sp, vp, vp, vp, i32, i32, f64, i32, u32, vp, vp, sz, vp]
-        L.ipv_compact.argtypes = [sp, vp, vp, vp, vp, i32, vp, i32, vp, sz, vp]
-        L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp]
-        L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, i32, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp,
+        ns = ctypes.POINTER(i32)  # host array of B row counts
+        L.ipv_tar_scores.argtypes = [sp, vp, vp, vp, ns, i32, u32, vp, vp, sz, vp]
+        L.ipv_van_scores.argtypes = [sp, vp, vp, vp, ns, vp, vp, vp, vp, sz, vp]
+        L.ipv_select.argtypes = [sp, vp, vp, vp, ns, i32, f64, i32, u32, vp, vp, sz, vp]
+        L.ipv_compact.argtypes = [sp, vp, vp, vp, vp, ns, vp, i32, vp, sz, vp]
+        L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, ns, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp]
+        L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, ns, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp,
                                          ctypes.POINTER(Events)]
-        L.ipv_append.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, vp]
-        L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f64, i32, u32, vp, vp, vp,
-                                   vp, vp, sz, ctypes.POINTER(i32), ctypes.POINTER(i32), vp]
+        L.ipv_append.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, vp]
+        L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, i32, i32, f64, i32, u32, vp, vp, vp,
+                                   vp, vp, sz, ns, ns, vp]
         L.ipv_clear_device_errors.argtypes = [vp, sz, vp]
         L.ipv_read_device_errors.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
         L.ipv_status_str.argtypes = [ctypes.c_int]
@@ -124,6 +125,17 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def counts(n_tokens, streams: int):
+    """Host array of per-stream row counts from an int (every stream) or a sequence."""
+    if isinstance(n_tokens, int):
+        vals = [n_tokens] * streams
+    else:
+        vals = [int(v) for v in n_tokens]
+        if len(vals) != streams:
+            raise IpvError(ERR_SHAPE, "n_tokens needs one count per stream (%d)" % streams)
+    return (ctypes.c_int32 * streams)(*vals)
+
+
 def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -143,7 +155,7 @@ def alloc_workspace(shape: Shape, device) -> torch.Tensor:
 
 def ipv_tar_scores(K, frame_idx, patch_idx, n_tokens, recent_frames, tar, ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
-    _check(lib().ipv_tar_scores(ctypes.byref(s), _ptr(K), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    _check(lib().ipv_tar_scores(ctypes.byref(s), _ptr(K), _ptr(frame_idx), _ptr(patch_idx), counts(n_tokens, s.streams),
                                 recent_frames, mode, _ptr(tar), _ptr(ws), ws.numel(), _stream(stream)),
            "ipv_tar_scores")
 
@@ -151,7 +163,7 @@ def ipv_tar_scores(K, frame_idx, patch_idx, n_tokens, recent_frames, tar, ws, gr
 def ipv_van_scores(V, frame_idx, patch_idx, n_tokens, cv_tau, van, pool_size, ws, grid_h, grid_w, stream=None):
     s = shape_of(V, grid_h, grid_w)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
-    _check(lib().ipv_van_scores(ctypes.byref(s), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    _check(lib().ipv_van_scores(ctypes.byref(s), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), counts(n_tokens, s.streams),
                                 None if tau is None else ctypes.addressof(tau), _ptr(van), _ptr(pool_size),
                                 _ptr(ws), ws.numel(), _stream(stream)), "ipv_van_scores")
 
@@ -162,7 +174,7 @@ def ipv_select(tar, van, frame_idx, n_tokens, budget, alpha, recent_frames, keep
     score tensors and the patch grid; head_dim/dtype only size the workspace."""
     B, L, H, S = tar.shape
     s = Shape(B, L, H, head_dim, S, grid_h, grid_w, dtype)
-    _check(lib().ipv_select(ctypes.byref(s), _ptr(tar), _ptr(van), _ptr(frame_idx), n_tokens, budget,
+    _check(lib().ipv_select(ctypes.byref(s), _ptr(tar), _ptr(van), _ptr(frame_idx), counts(n_tokens, B), budget,
                             float(alpha), recent_frames, mode, _ptr(keep_idx), _ptr(ws), ws.numel(),
                             _stream(stream)),
            "ipv_select")
@@ -170,7 +182,8 @@ def ipv_select(tar, van, frame_idx, n_tokens, budget, alpha, recent_frames, keep
 
 def ipv_compact(K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, grid_h, grid_w, stream=None):
     s = shape_of(K, grid_h, grid_w)
-    _check(lib().ipv_compact(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    _check(lib().ipv_compact(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
+                             counts(n_tokens, s.streams),
                              _ptr(keep_idx), budget, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)),
            "ipv_compact")
 
@@ -179,7 +192,8 @@ def ipv_compress(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_fra
                  ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
-    _check(lib().ipv_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    _check(lib().ipv_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
+                              counts(n_tokens, s.streams),
                               budget, float(alpha), recent_frames, mode, None if tau is None else ctypes.addressof(tau),
                               _ptr(tar), _ptr(van), _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream)),
            "ipv_compress")
@@ -189,7 +203,8 @@ def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, rece
                        keep_idx, ws, grid_h, grid_w, events: Events, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
-    _check(lib().ipv_compress_timed(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    _check(lib().ipv_compress_timed(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
+                                    counts(n_tokens, s.streams),
                                     budget, float(alpha), recent_frames, mode,
                                     None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
                                     _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(events)),
@@ -197,36 +212,42 @@ def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, rece
 
 
 def ipv_append(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, first_patch, grid_h, grid_w,
-               stream=None) -> int:
-    """Append K_new/V_new ([B, L, H, rows, D]) after row n_tokens of every
-    slice; returns the new row count."""
+               stream=None):
+    """Append K_new/V_new ([B, L, H, rows, D]) after row n_tokens[b] of every
+    slice of stream b; returns the new row count(s) (an int for an int
+    n_tokens, else a list)."""
     s = shape_of(K, grid_h, grid_w)
     if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
             or K_new.shape[4] != K.shape[4] or K_new.dtype != K.dtype:
         raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
     rows = K_new.shape[3]
-    _check(lib().ipv_append(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    ns = counts(n_tokens, s.streams)
+    _check(lib().ipv_append(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), ns,
                             _ptr(K_new), _ptr(V_new), rows, frame_id, first_patch, _stream(stream)), "ipv_append")
-    return n_tokens + rows
+    return n_tokens + rows if isinstance(n_tokens, int) else [v + rows for v in ns]
 
 
 def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, first_patch, mem_cap, budget,
                  alpha, recent_frames, cv_tau, tar, van, keep_idx, ws, grid_h, grid_w, stream=None, mode=0):
-    """Append, then compress to `budget` once the cache holds >= mem_cap rows.
-    Returns (new row count, whether the pass ran)."""
+    """Append, then compress to `budget` every stream that holds >= mem_cap
+    rows. Returns (row counts, whether each stream's pass ran): ints for an
+    int n_tokens (every stream then behaves alike), else lists."""
     s = shape_of(K, grid_h, grid_w)
     if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
             or K_new.shape[4] != K.shape[4] or K_new.dtype != K.dtype:
         raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
-    n_out, comp = ctypes.c_int32(0), ctypes.c_int32(0)
-    _check(lib().ipv_ckv_step(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), n_tokens,
+    n_out, comp = (ctypes.c_int32 * s.streams)(), (ctypes.c_int32 * s.streams)()
+    _check(lib().ipv_ckv_step(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
+                              counts(n_tokens, s.streams),
                               _ptr(K_new), _ptr(V_new), K_new.shape[3], frame_id, first_patch, mem_cap, budget,
                               float(alpha), recent_frames, mode, None if tau is None else ctypes.addressof(tau),
                               _ptr(tar),
                               _ptr(van), _ptr(keep_idx), _ptr(ws), 0 if ws is None else ws.numel(),
-                              ctypes.byref(n_out), ctypes.byref(comp), _stream(stream)), "ipv_ckv_step")
-    return n_out.value, bool(comp.value)
+                              n_out, comp, _stream(stream)), "ipv_ckv_step")
+    if isinstance(n_tokens, int):
+        return n_out[0], bool(comp[0])
+    return list(n_out), [bool(c) for c in comp]
 
 
 def ipv_clear_device_errors(ws, stream=None):

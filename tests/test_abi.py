@@ -40,6 +40,11 @@ SEVEN_B = dict(streams=1, layers=28, kv_heads=4, head_dim=128, capacity=6272, gr
 FAKE = 0x10000  # a 256-aligned non-null address; never dereferenced because another argument is rejected
 
 
+def N(*vals):
+    """Host array of per-stream row counts."""
+    return (ctypes.c_int32 * len(vals))(*vals)
+
+
 def shape(**kw):
     d = dict(SEVEN_B)
     d.update(kw)
@@ -68,7 +73,8 @@ def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, w
         p.update(ptrs)
     t = None if tau is None else (ctypes.c_double * 3)(*tau)
     wsb = wsb if wsb is not None else 0  # default: workspace too small
-    return ipv.lib().ipv_compress(ctypes.byref(s), p["K"], p["V"], p["fr"], p["pa"], n, budget, alpha, r, mode,
+    ns = N(*([n] * s.streams)) if isinstance(n, int) else N(*n)
+    return ipv.lib().ipv_compress(ctypes.byref(s), p["K"], p["V"], p["fr"], p["pa"], ns, budget, alpha, r, mode,
                                   None if t is None else ctypes.addressof(t), p["tar"], p["van"], p["keep"], ws,
                                   wsb, None)
 
@@ -78,7 +84,7 @@ def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, w
     (dict(ptrs=dict(keep=None)), ipv.ERR_NULL),
     (dict(ptrs=dict(V=FAKE + 8)), ipv.ERR_ALIGN),
     (dict(ptrs=dict(tar=FAKE + 4)), ipv.ERR_ALIGN),
-    (dict(n=0), ipv.ERR_SHAPE),
+    (dict(n=-1), ipv.ERR_SHAPE),
     (dict(n=6273), ipv.ERR_SHAPE),                # n > capacity
     (dict(budget=6273), ipv.ERR_BUDGET),          # budget > n
     (dict(budget=783), ipv.ERR_BUDGET),           # smaller than r * p
@@ -123,21 +129,21 @@ def test_rows_above_select_limit_rejected():
 def test_entry_points_validate_their_own_arguments():
     L, s = ipv.lib(), shape()
     big = 1 << 40
-    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 0, 0, FAKE, FAKE, big, None) == ipv.ERR_ARG
-    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, None, FAKE, 6272, 4, 0, FAKE, FAKE, big, None) == ipv.ERR_NULL
-    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 4, 32, FAKE, FAKE, big, None) == ipv.ERR_ARG
-    assert L.ipv_van_scores(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, None, FAKE, FAKE + 2, FAKE, big,
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 0, 0, FAKE, FAKE, big, None) == ipv.ERR_ARG
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, None, FAKE, N(6272), 4, 0, FAKE, FAKE, big, None) == ipv.ERR_NULL
+    assert L.ipv_tar_scores(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 4, 32, FAKE, FAKE, big, None) == ipv.ERR_ARG
+    assert L.ipv_van_scores(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), None, FAKE, FAKE + 2, FAKE, big,
                             None) == ipv.ERR_ALIGN
-    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 3136, -0.1, 4, 0, FAKE, FAKE, big,
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 3136, -0.1, 4, 0, FAKE, FAKE, big,
                         None) == ipv.ERR_ARG
-    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 100, 0.5, 4, 0, FAKE, FAKE, big,
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 100, 0.5, 4, 0, FAKE, FAKE, big,
                         None) == ipv.ERR_BUDGET
-    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, 6272, 3136, 0.5, 4, 64, FAKE, FAKE, big,
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 3136, 0.5, 4, 64, FAKE, FAKE, big,
                         None) == ipv.ERR_ARG
-    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE, 0, None, 0, None) == ipv.ERR_BUDGET
-    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE + 4, 10, None, 0,
+    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(6272), FAKE, 0, None, 0, None) == ipv.ERR_BUDGET
+    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(6272), FAKE + 4, 10, None, 0,
                          None) == ipv.ERR_ALIGN
-    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6272, FAKE, 10, FAKE, 8, None) == ipv.ERR_WORKSPACE
+    assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(6272), FAKE, 10, FAKE, 8, None) == ipv.ERR_WORKSPACE
     assert L.ipv_clear_device_errors(None, 256, None) == ipv.ERR_NULL
     assert L.ipv_clear_device_errors(FAKE, 8, None) == ipv.ERR_WORKSPACE
     out = ctypes.c_uint32()
@@ -156,17 +162,16 @@ def test_append_and_ckv_step_validate_before_launch():
     L, s = ipv.lib(), shape()
     big = 1 << 40
     # ipv_append(shape, K, V, fr, pa, n, K_new, V_new, rows, frame_id, first_patch, stream)
-    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, None, FAKE, 196, 0, 0, None) == ipv.ERR_NULL
-    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE + 4, FAKE, 196, 0, 0, None) == ipv.ERR_ALIGN
-    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 6200, FAKE, FAKE, 196, 0, 0, None) == ipv.ERR_SHAPE
-    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, 0, 0, 0, None) == ipv.ERR_SHAPE
-    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, 100, 0, 97, None) == ipv.ERR_ARG
-    n_out, comp = ctypes.c_int32(), ctypes.c_int32()
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(0), None, FAKE, 196, 0, 0, None) == ipv.ERR_NULL
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(0), FAKE + 4, FAKE, 196, 0, 0, None) == ipv.ERR_ALIGN
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(6200), FAKE, FAKE, 196, 0, 0, None) == ipv.ERR_SHAPE
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(0), FAKE, FAKE, 0, 0, 0, None) == ipv.ERR_SHAPE
+    assert L.ipv_append(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(0), FAKE, FAKE, 100, 0, 97, None) == ipv.ERR_ARG
+    n_out, comp = N(0), N(0)
 
     def step(n=6076, rows=196, cap=6272, budget=3136, tar=FAKE, ws=FAKE, wsb=big, nout=True, mode=0):
-        return L.ipv_ckv_step(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, n, FAKE, FAKE, rows, 30, 0, cap, budget, 0.5,
-                              4, mode, None, tar, FAKE, FAKE, ws, wsb, ctypes.byref(n_out) if nout else None,
-                              ctypes.byref(comp), None)
+        return L.ipv_ckv_step(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(n), FAKE, FAKE, rows, 30, 0, cap, budget, 0.5,
+                              4, mode, None, tar, FAKE, FAKE, ws, wsb, n_out if nout else None, comp, None)
 
     assert step(nout=False) == ipv.ERR_NULL
     assert step(n=6272) == ipv.ERR_SHAPE          # the previous step left the cache at the cap
@@ -176,3 +181,20 @@ def test_append_and_ckv_step_validate_before_launch():
     assert step(wsb=0) == ipv.ERR_WORKSPACE
     assert step(budget=700) == ipv.ERR_BUDGET     # smaller than the recent window
     assert step(mode=128) == ipv.ERR_ARG          # unknown mode bit
+
+
+def test_per_stream_row_counts_are_validated_before_launch():
+    s = shape(streams=3)
+    big = 1 << 40
+    assert call_compress(s, n=[6272, 6272, 7000], wsb=big) == ipv.ERR_SHAPE     # a count above the capacity
+    assert call_compress(s, n=[6272, -1, 6272], wsb=big) == ipv.ERR_SHAPE
+    assert call_compress(s, n=[6272, 3000, 6272], wsb=big) == ipv.ERR_BUDGET    # budget above one stream's rows
+    L = ipv.lib()
+    assert L.ipv_compress(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, None, 3136, 0.5, 4, 0, None, FAKE, FAKE, FAKE,
+                          FAKE, big, None) == ipv.ERR_NULL
+
+
+def test_every_stream_empty_is_a_no_op():
+    # no stream has rows: every argument is checked, nothing is launched
+    s = shape(streams=2)
+    assert call_compress(s, n=[0, 0], wsb=1 << 40) == ipv.OK
