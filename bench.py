@@ -10,6 +10,7 @@ timing. Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 7b-class-28L]
                   [--mode tar_reverse,van_reverse,tar_adjacent,head_shared]
+  python bench.py --workload streaming-16x16 --stream   # the whole frame stream through ipv_ckv_step
 """
 from __future__ import annotations
 
@@ -207,6 +208,8 @@ def main():
     ap.add_argument("--workload", default=W.SEVEN_B.name)
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--mode", default="", help="comma-separated variant modes (default: the method as published)")
+    ap.add_argument("--stream", action="store_true",
+                    help="streaming workloads: time whole frame streams through ipv_ckv_step (steps = streams)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-calibration copy")
@@ -236,6 +239,9 @@ def main():
     w = W.BY_NAME[args.workload]
     alpha = w.alphas[0] if args.alpha is None else args.alpha
     mode = parse_mode(args.mode)
+    if args.stream:
+        stream_main(args, w, alpha, mode)
+        return
     names = STEP_NAMES_ADJACENT if mode & MODE_BITS["tar_adjacent"] else STEP_NAMES
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -354,6 +360,123 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, K, V, fr, pa, alpha, args.cpu_seconds, mode)
+    print(json.dumps(out), flush=True)
+
+
+def stream_main(args, w, alpha, mode):
+    """The workload's whole frame stream, one frame per ipv_ckv_step (append,
+    and the pass whenever a stream reaches the cap). All frames are resident
+    in HBM before timing; each timed step is one whole stream from an empty
+    cache; events bracket every step that runs the pass."""
+    import torch
+    from paper_2506_15745_amd import ipv
+
+    if not w.stream_frames:
+        raise SystemExit("--stream needs a streaming workload")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    hip = Hip()
+    p, F, L, H, D = w.p, w.stream_frames, w.layers, w.kv_heads, w.head_dim
+    kind = torch.bfloat16 if w.dtype == synth.BF16 else torch.float32
+    st = synth.Stream(w.seeds[0], L, H, F * p, D, w.grid_h, w.grid_w, w.dtype, w.rho_specs[0], tuple(w.value_sigma))
+    st.append(F)
+
+    def frames_of(a):  # [L, H, F*p, D] host -> [F, 1, L, H, p, D] device, frame-major
+        t = torch.from_numpy(a)
+        t = (t.view(kind) if kind == torch.bfloat16 else t).to(dev)
+        return t.view(L, H, F, p, D).permute(2, 0, 1, 3, 4).contiguous().unsqueeze(1)
+
+    Kf, Vf = frames_of(st.K), frames_of(st.V)
+    del st
+    cap, C = w.n_tokens, w.budget
+    S = cap + p
+    Kd = torch.zeros((1, L, H, S, D), dtype=kind, device=dev)
+    Vd = torch.zeros_like(Kd)
+    fd = torch.full((1, L, H, S), -1, dtype=torch.int32, device=dev)
+    pd = torch.full_like(fd, -1)
+    comp = ipv.Compressor(Kd, w.grid_h, w.grid_w, C)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    # which steps run the pass (the trigger is a host-side count)
+    fires, n = [], 0
+    for f in range(F):
+        n += p
+        fires.append(n >= cap)
+        n = C if n >= cap else n
+    passes = sum(fires)
+    ev = [[(hip.event(), hip.event()) for _ in range(passes)] for _ in range(args.steps)]
+    stream_ev = [(hip.event(), hip.event()) for _ in range(args.steps)]
+    record = hip.lib.hipEventRecord
+    record.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+
+    def one_stream(events=None, bracket=None):
+        n = 0
+        k = 0
+        cur = torch.cuda.current_stream().cuda_stream
+        if bracket:
+            record(bracket[0], cur)
+        for f in range(F):
+            if events and fires[f]:
+                record(events[k][0], cur)
+            n, fired = ipv.ipv_ckv_step(Kd, Vd, fd, pd, n, Kf[f], Vf[f], f, 0, cap, C, alpha, w.recent_frames,
+                                        w.cv_tau, comp.tar, comp.van, comp.keep_idx, comp.ws, w.grid_h, w.grid_w,
+                                        mode=mode)
+            if events and fired:
+                record(events[k][1], cur)
+                k += 1
+        if bracket:
+            record(bracket[1], cur)
+
+    flush.fill_(1.0)
+    flush.sum()
+    for _ in range(args.warmup):
+        one_stream()
+    torch.cuda.synchronize()
+    flush.fill_(2.0)
+    flush.sum()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        one_stream(ev[i], stream_ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    errors = comp.device_errors()
+    pass_us = [hip.elapsed_ms(a, b) * 1e3 for run in ev for a, b in run]
+    stream_ms = [hip.elapsed_ms(a, b) for a, b in stream_ev]
+    pass_mean = statistics.mean(pass_us)
+    algo = w.algorithmic_bytes()
+    value = algo / (pass_mean * 1e-6) / 1e9
+    stream_mean = statistics.mean(stream_ms)
+    append_us = (stream_mean * 1e3 - sum(pass_us) / args.steps) / (F - passes)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == synth.BF16 else "f32",
+        "data": "synthetic (seeded AR(1) keys, log-normal-scaled values)",
+        "config": {"workload": w.name, "streams": 1, "layers": L, "kv_heads": H, "head_dim": D,
+                   "tokens_per_frame": p, "frames": F, "mem_cap": cap, "budget": C,
+                   "recent_frames": w.recent_frames, "alpha": alpha, "parallelism": "single GPU",
+                   "step": "one whole stream through ipv_ckv_step", **({"mode": args.mode} if mode else {})},
+        "latency_us": {"pass_mean": round(pass_mean, 2), "pass_p50": round(pct(pass_us, 0.5), 2),
+                       "pass_p99": round(pct(pass_us, 0.99), 2)},
+        "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
+        "stream": {"passes_per_stream": passes, "stream_ms_mean": round(stream_mean, 3),
+                   "compression_ms_per_stream": round(sum(pass_us) / args.steps / 1e3, 3),
+                   "append_us_mean": round(append_us, 2),
+                   "tokens_per_s": round(F * p / (stream_mean * 1e-3), 1)},
+        "algorithmic_bytes_per_pass": algo,
+        "roofline": {"bound": "hbm", "kernel": "whole pass (ipv_ckv_step that fires)", "achieved": round(value, 1),
+                     "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(value / PEAK_HBM_GBPS, 4),
+                     "algorithmic_bytes": algo, "traffic": None},
+        "device_errors": errors,
+    }
     print(json.dumps(out), flush=True)
 
 
