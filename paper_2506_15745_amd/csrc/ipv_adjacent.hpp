@@ -193,30 +193,13 @@ __global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K,
   float tsc[U], vsc[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    float a[EPL], c[EPL];
-    Lane<T>::decode(kx[u], a);
-    Lane<T>::decode(ky[u], c);
-    float dot = 0.f, aa = 0.f, cc = 0.f;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      dot += a[i] * c[i];
-      aa += a[i] * a[i];
-      cc += c[i] * c[i];
-    }
-    dot = group_sum<LPR>(dot);
-    aa = group_sum<LPR>(aa);
-    cc = group_sum<LPR>(cc);
-    float sc = (y[u] >= 0 && aa > 0.f && cc > 0.f) ? -(dot / (sqrtf(aa) * sqrtf(cc))) : 0.f;
+    const float dot = group_sum<LPR>(Lane<T>::dot(kx[u], ky[u]));
+    const float aa = group_sum<LPR>(Lane<T>::sumsq(kx[u]));
+    const float cc = group_sum<LPR>(Lane<T>::sumsq(ky[u]));
+    float sc = (y[u] >= 0 && aa > 0.f && cc > 0.f) ? -(dot * fast_rsqrt(aa) * fast_rsqrt(cc)) : 0.f;
     if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
     tsc[u] = sc;
-    if (VAN) {
-      float v[EPL];
-      Lane<T>::decode(vx[u], v);
-      float ss = 0.f;
-#pragma unroll
-      for (int i = 0; i < EPL; ++i) ss += v[i] * v[i];
-      vsc[u] = sqrtf(group_sum<LPR>(ss));
-    }
+    if (VAN) vsc[u] = fast_sqrt(group_sum<LPR>(Lane<T>::sumsq(vx[u])));
   }
   if (lane < U) {
     const int64_t x = r0 + lane * GROUPS + g;

@@ -16,8 +16,13 @@ struct alignas(16) Raw16 {
 };
 
 // 16 bytes of a row, decoded to fp32. EPL = elements per 16-byte lane chunk.
+// dot / sumsq: the dot product of two 16-byte chunks / the sum of squares of
+// one, accumulated in fp32 (bf16 pairs by the packed bf16 dot instruction:
+// each bf16 product is exact in fp32).
 template <typename T>
 struct Lane;
+
+typedef __bf16 Bf16x2 __attribute__((ext_vector_type(2)));
 
 template <>
 struct Lane<uint16_t> {  // bf16 bit patterns
@@ -29,6 +34,15 @@ struct Lane<uint16_t> {  // bf16 bit patterns
       f[2 * i + 1] = __uint_as_float(r.w[i] & 0xffff0000u);
     }
   }
+  __device__ static inline float dot(const Raw16& a, const Raw16& b) {
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(Bf16x2, a.w[i]), __builtin_bit_cast(Bf16x2, b.w[i]),
+                                            acc, false);
+    return acc;
+  }
+  __device__ static inline float sumsq(const Raw16& r) { return dot(r, r); }
 };
 
 template <>
@@ -38,7 +52,19 @@ struct Lane<float> {
 #pragma unroll
     for (int i = 0; i < 4; ++i) f[i] = __uint_as_float(r.w[i]);
   }
+  __device__ static inline float dot(const Raw16& a, const Raw16& b) {
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc += __uint_as_float(a.w[i]) * __uint_as_float(b.w[i]);
+    return acc;
+  }
+  __device__ static inline float sumsq(const Raw16& r) { return dot(r, r); }
 };
+
+// Hardware square root and reciprocal square root (about 1 ulp): the scores
+// need 1e-3 relative accuracy, not the correctly rounded sequences.
+__device__ inline float fast_sqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
+__device__ inline float fast_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
 
 __device__ inline Raw16 load16(const void* p) { return *reinterpret_cast<const Raw16*>(p); }
 

@@ -130,11 +130,8 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
         ++cnt;
         float f[EPL];
         Lane<T>::decode(raw[b], f);
-        float ss = 0.f;
-#pragma unroll
-        for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
-        ss = group_sum<LPR>(ss);
-        const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+        const float ss = group_sum<LPR>(Lane<T>::sumsq(raw[b]));
+        const float inv = ss > 0.f ? fast_rsqrt(ss) : 0.f;
 #pragma unroll
         for (int i = 0; i < EPL; ++i) acc[i] += f[i] * inv;
       }
@@ -271,14 +268,8 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t x = (int64_t)(f0 + u) * p + col;
-      float f[EPL];
-      float ss = 0.f;
-      if (x < n) {
-        Lane<T>::decode(vr[u], f);
-#pragma unroll
-        for (int i = 0; i < EPL; ++i) ss += f[i] * f[i];
-      }
-      vsc[u] = sqrtf(group_sum<LPR>(ss));
+      const float ss = x < n ? Lane<T>::sumsq(vr[u]) : 0.f;
+      vsc[u] = fast_sqrt(group_sum<LPR>(ss));
     }
   }
   if (TAR) {
@@ -304,12 +295,12 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
         for (int i = 0; i < EPL; i += 4) {
           const float4 mv = m[i / 4];
           dot += f[i] * mv.x + f[i + 1] * mv.y + f[i + 2] * mv.z + f[i + 3] * mv.w;
-          kk += f[i] * f[i] + f[i + 1] * f[i + 1] + f[i + 2] * f[i + 2] + f[i + 3] * f[i + 3];
         }
+        kk = Lane<T>::sumsq(kr[u]);
       }
       dot = group_sum<LPR>(dot);
       kk = group_sum<LPR>(kk);
-      float sc = kk > 0.f ? -(dot / sqrtf(kk)) : 0.f;
+      float sc = kk > 0.f ? -(dot * fast_rsqrt(kk)) : 0.f;
       if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
       tsc[u] = past ? sc : 0.f;
     }
