@@ -198,3 +198,24 @@ def test_every_stream_empty_is_a_no_op():
     # no stream has rows: every argument is checked, nothing is launched
     s = shape(streams=2)
     assert call_compress(s, n=[0, 0], wsb=1 << 40) == ipv.OK
+
+
+def test_binding_row_counts():
+    assert list(ipv.counts(6272, 3)) == [6272, 6272, 6272]
+    assert list(ipv.counts([1, 2, 3], 3)) == [1, 2, 3]
+    with pytest.raises(ipv.IpvError):
+        ipv.counts([1, 2], 3)
+
+
+def test_ckv_step_checks_every_stream():
+    s = shape(streams=2)
+    L, big = ipv.lib(), 1 << 40
+    n_out, comp = N(0, 0), N(0, 0)
+
+    def step(counts, budget=3136):
+        return L.ipv_ckv_step(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(*counts), FAKE, FAKE, 196, 30, 0, 6272,
+                              budget, 0.5, 4, 0, None, FAKE, FAKE, FAKE, FAKE, big, n_out, comp, None)
+
+    assert step([100, 6272]) == ipv.ERR_SHAPE        # one stream is already at the cap
+    assert step([100, -4]) == ipv.ERR_SHAPE
+    assert step([6076, 100], budget=700) == ipv.ERR_BUDGET  # stream 0 would run the pass: its budget is checked
