@@ -48,9 +48,6 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
   const int32_t q = q0 + g;
   const int64_t t0 = max((int64_t)0, (int64_t)n - (int64_t)r * p);
 
-  for (int i = tid; i < GROUPS * r; i += NT) slot[i] = -1;
-  __syncthreads();
-
   // Loads take clamped (in-range) indices instead of branches, so that they
   // are all in flight together; values of clamped loads are never used. The
   // window scan reads NT * kScanBatch rows per batch (the whole window in the
@@ -97,6 +94,9 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
     const int64_t x = min(t0 + (int64_t)j * p + q, (int64_t)n - 1);
     spec[j] = load16(K + (base + x) * D + lane * EPL);
   }
+  // the slot table is cleared while the loads are in flight
+  for (int i = tid; i < GROUPS * r; i += NT) slot[i] = -1;
+  __syncthreads();
   scan_batch(t0);
   for (int64_t tb = t0 + (int64_t)NT * kScanBatch; tb < n; tb += (int64_t)NT * kScanBatch) {
     load_batch(tb);
