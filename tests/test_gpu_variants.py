@@ -152,3 +152,13 @@ def test_head_shared_flags_heads_with_different_frames():
     assert got.errors & ipv.DEV_BAD_FRAMES
     # the documented fallback: every head keeps rows 0..C-1
     assert np.array_equal(got.keep[0, 0], np.tile(np.arange(w.budget, dtype=np.int32), (2, 1)))
+
+
+@pytest.mark.parametrize("mode", [0, ipv.TAR_ADJACENT | ipv.TAR_REVERSE])
+def test_rows_up_to_the_selection_limit(mode):
+    # 64 rows per thread in the selection (n > 32768) and 50 chunks of the prev-row walk
+    gh = gw = 16
+    n = 50000
+    st = synth.fresh_cache(29, 1, 2, n + 3, 64, gh, gw, n, synth.BF16, synth.RhoSpec(0.0, 0.99, 0.3))
+    mode_check("n50000", st.K[None], st.V[None], st.frame_idx[None], st.patch_idx[None], n, 20000, 0.5, 6, gh, gw,
+               mode)
