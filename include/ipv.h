@@ -17,6 +17,7 @@
  *   ipv_compress     the four steps above, in order, on one stream
  *   ipv_append       add a frame's rows to the cache (Algorithm 1 step (1))
  *   ipv_ckv_step     append, then compress when the memory cap is reached
+ *   ipv_ckv_stream   many frames through that loop in one call
  *
  * A `mode` argument (IPV_MODE_* bits, 0 = the method as published) selects the
  * variants of the paper's ablation (Tab. 5: TaR Reverse, VaN Reverse, TaR
@@ -250,6 +251,23 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
                         int32_t first_patch, int32_t mem_cap, int32_t budget, double alpha, int32_t recent_frames,
                         uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx, void* ws, size_t ws_bytes,
                         int32_t* n_out, int32_t* compressed, void* stream);
+
+/*
+ * A whole stretch of a stream through the loop above, driven from the host
+ * library with no round trip per frame: for f = 0 .. n_frames-1, the
+ * equivalent of ipv_ckv_step with K_new / V_new = frame f of frames_K /
+ * frames_V ([n_frames, B, L, H, rows, D], device, 16-byte aligned), frame id
+ * first_frame_id + f and first_patch 0. n_tokens (host, [B]) holds the row
+ * counts on entry and receives them on return; passes (host, [B]) receives how
+ * many times each stream was compressed. Every step is checked before the
+ * first is enqueued (the counts of the whole stretch follow from the counts,
+ * rows, mem_cap and budget), so a rejected call enqueues nothing.
+ */
+ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                          int32_t* n_tokens, const void* frames_K, const void* frames_V, int32_t n_frames,
+                          int32_t rows, int32_t first_frame_id, int32_t mem_cap, int32_t budget, double alpha,
+                          int32_t recent_frames, uint32_t mode, const double* cv_tau, float* tar, float* van,
+                          int32_t* keep_idx, void* ws, size_t ws_bytes, int32_t* passes, void* stream);
 
 /* Reset the workspace's device error word (a small kernel on `stream`). */
 ipv_status ipv_clear_device_errors(void* ws, size_t ws_bytes, void* stream);

@@ -585,6 +585,57 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
   return IPV_OK;
 }
 
+ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                          int32_t* n_tokens, const void* frames_K, const void* frames_V, int32_t n_frames,
+                          int32_t rows, int32_t first_frame_id, int32_t mem_cap, int32_t budget, double alpha,
+                          int32_t recent_frames, uint32_t mode, const double* cv_tau, float* tar, float* van,
+                          int32_t* keep_idx, void* ws, size_t ws_bytes, int32_t* passes, void* stream) {
+  Dims d;
+  IPV_TRY(check_shape(shape, &d));
+  if (!n_tokens || !passes || !frames_K || !frames_V || !K || !V || !frame_idx || !patch_idx) return IPV_ERR_NULL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
+      !aligned(frames_K, 16) || !aligned(frames_V, 16))
+    return IPV_ERR_ALIGN;
+  if (n_frames < 0 || rows < 1 || mem_cap < 1 || mem_cap > d.S) return IPV_ERR_SHAPE;
+  if (budget > mem_cap) return IPV_ERR_BUDGET;
+  if ((int64_t)first_frame_id + n_frames > INT32_MAX || rows > d.p) return IPV_ERR_ARG;
+  // every step is checked on the host before the first one is enqueued: the
+  // row counts of the whole stretch follow from the counts, rows and cap alone
+  std::vector<int32_t> n(n_tokens, n_tokens + d.B), after((size_t)d.B), pass((size_t)d.B);
+  bool any_pass = false;
+  for (int32_t f = 0; f < n_frames; ++f) {
+    bool any = false;
+    for (int64_t b = 0; b < d.B; ++b) {
+      if (n[b] < 0 || n[b] >= mem_cap || (int64_t)n[b] + rows > d.S) return IPV_ERR_SHAPE;
+      after[b] = n[b] + rows;
+      pass[b] = after[b] >= mem_cap ? after[b] : 0;
+      any |= pass[b] > 0;
+    }
+    if (any) IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode));
+    any_pass |= any;
+    for (int64_t b = 0; b < d.B; ++b) n[b] = pass[b] > 0 ? budget : after[b];
+  }
+  if (any_pass) {
+    if (!tar || !van || !keep_idx) return IPV_ERR_NULL;
+    if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
+    IPV_TRY(check_ws(d, ws, ws_bytes));
+  }
+  const size_t frame_bytes = (size_t)(d.slices * rows * d.D * d.elem);
+  for (int64_t b = 0; b < d.B; ++b) passes[b] = 0;
+  std::vector<int32_t> n_out((size_t)d.B), fired((size_t)d.B);
+  for (int32_t f = 0; f < n_frames; ++f) {
+    IPV_TRY(ipv_ckv_step(shape, K, V, frame_idx, patch_idx, n_tokens, static_cast<const char*>(frames_K) + f * frame_bytes,
+                         static_cast<const char*>(frames_V) + f * frame_bytes, rows, first_frame_id + f, 0, mem_cap,
+                         budget, alpha, recent_frames, mode, cv_tau, tar, van, keep_idx, ws, ws_bytes, n_out.data(),
+                         fired.data(), stream));
+    for (int64_t b = 0; b < d.B; ++b) {
+      n_tokens[b] = n_out[b];
+      passes[b] += fired[b];
+    }
+  }
+  return IPV_OK;
+}
+
 ipv_status ipv_clear_device_errors(void* ws, size_t ws_bytes, void* stream) {
   if (!ws) return IPV_ERR_NULL;
   if (!aligned(ws, 256)) return IPV_ERR_ALIGN;

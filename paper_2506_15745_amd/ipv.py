@@ -31,7 +31,8 @@ DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN, DEV_WAIT_
 TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED = 1, 2, 4, 8
 
 EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
-           "ipv_compress", "ipv_compress_timed", "ipv_append", "ipv_ckv_step", "ipv_clear_device_errors",
+           "ipv_compress", "ipv_compress_timed", "ipv_append", "ipv_ckv_step", "ipv_ckv_stream",
+           "ipv_clear_device_errors",
            "ipv_read_device_errors", "ipv_status_str")
 
 
@@ -81,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.ipv_append.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, vp]
         L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, i32, i32, f64, i32, u32, vp, vp, vp,
                                    vp, vp, sz, ns, ns, vp]
+        L.ipv_ckv_stream.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, i32, i32, f64, i32, u32, vp, vp,
+                                     vp, vp, vp, sz, ns, vp]
         L.ipv_clear_device_errors.argtypes = [vp, sz, vp]
         L.ipv_read_device_errors.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
         L.ipv_status_str.argtypes = [ctypes.c_int]
@@ -248,6 +251,28 @@ def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, f
     if isinstance(n_tokens, int):
         return n_out[0], bool(comp[0])
     return list(n_out), [bool(c) for c in comp]
+
+
+def ipv_ckv_stream(K, V, frame_idx, patch_idx, n_tokens, frames_K, frames_V, first_frame_id, mem_cap, budget,
+                   alpha, recent_frames, cv_tau, tar, van, keep_idx, ws, grid_h, grid_w, stream=None, mode=0):
+    """Frames frames_K/V[f] ([F, B, L, H, rows, D]) through ipv_ckv_step one
+    after another in one library call. Returns (row counts, passes per
+    stream): ints for an int n_tokens, else lists."""
+    s = shape_of(K, grid_h, grid_w)
+    if frames_K.shape != frames_V.shape or frames_K.dim() != 6 or frames_K.shape[1:4] != K.shape[:3] \
+            or frames_K.shape[5] != K.shape[4] or frames_K.dtype != K.dtype:
+        raise IpvError(ERR_SHAPE, "frames_K/V must be [F, B, L, H, rows, D] like the cache")
+    tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
+    ns = counts(n_tokens, s.streams)
+    passes = (ctypes.c_int32 * s.streams)()
+    _check(lib().ipv_ckv_stream(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), ns,
+                                _ptr(frames_K), _ptr(frames_V), frames_K.shape[0], frames_K.shape[4], first_frame_id,
+                                mem_cap, budget, float(alpha), recent_frames, mode,
+                                None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van), _ptr(keep_idx),
+                                _ptr(ws), 0 if ws is None else ws.numel(), passes, _stream(stream)), "ipv_ckv_stream")
+    if isinstance(n_tokens, int):
+        return ns[0], passes[0]
+    return list(ns), list(passes)
 
 
 def ipv_clear_device_errors(ws, stream=None):

@@ -219,3 +219,22 @@ def test_ckv_step_checks_every_stream():
     assert step([100, 6272]) == ipv.ERR_SHAPE        # one stream is already at the cap
     assert step([100, -4]) == ipv.ERR_SHAPE
     assert step([6076, 100], budget=700) == ipv.ERR_BUDGET  # stream 0 would run the pass: its budget is checked
+
+
+def test_ckv_stream_checks_every_step_before_launch():
+    s = shape(streams=1)
+    L, big = ipv.lib(), 1 << 40
+    passes = N(0)
+
+    def run(n=0, frames=40, tar=FAKE, budget=3136, wsb=big, cap=6272, counts=True):
+        return L.ipv_ckv_stream(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(n) if counts else None, FAKE, FAKE,
+                                frames, 196, 0, cap, budget, 0.5, 4, 0, None, tar, FAKE, FAKE, FAKE, wsb, passes,
+                                None)
+
+    assert run(counts=False) == ipv.ERR_NULL
+    assert run(tar=None) == ipv.ERR_NULL          # the pass at step 31 would need it: rejected up front
+    assert run(wsb=0) == ipv.ERR_WORKSPACE
+    assert run(budget=600) == ipv.ERR_BUDGET      # below the recent window at the first pass
+    assert run(n=6272) == ipv.ERR_SHAPE           # already at the cap
+    assert run(cap=7000) == ipv.ERR_SHAPE
+    assert run(frames=0) == ipv.OK and passes[0] == 0    # nothing to do, nothing launched
