@@ -35,7 +35,8 @@ METRIC = "compression-pass latency (us) + achieved HBM GB/s (% of peak), 1 MI355
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = os.path.join(ROOT, "paper_2506_15745_amd", "csrc")
 PEAK_HBM_GBPS = 8000.0
-STEP_NAMES = ("recent_table", "score_sweep", "pool", "select", "compact")
+# the recent-key table runs in one launch with the VaN tiles; the TaR tiles follow
+STEP_NAMES = ("table_van", "tar_sweep", "pool", "select", "compact")
 # with consecutive-frame TaR the first two steps are the prev-row walk and the adjacent sweep
 STEP_NAMES_ADJACENT = ("prev_walk", "adjacent_sweep", "pool", "select", "compact")
 MODE_BITS = {"tar_reverse": 1, "van_reverse": 2, "tar_adjacent": 4, "head_shared": 8}
@@ -153,7 +154,7 @@ def summarize(paths):
                                                           name[:110]))
 
 
-STEP_KERNELS = {"recent_table": "k_recent_table<", "score_sweep": "k_score_sweep<", "select": "k_select<",
+STEP_KERNELS = {"table_van": "k_table_van<", "tar_sweep": "k_score_sweep<", "select": "k_select<",
                 "compact": "k_compact<"}
 
 
@@ -322,10 +323,16 @@ def main():
     n_recent = min(w.n_tokens, w.recent_frames * w.p)
     if w.n_tokens % w.p:
         n_recent = (w.recent_frames - 1) * w.p + w.n_tokens % w.p
-    algo_by_step = {"recent_table": B * L * H * n_recent * row,
-                    names[1]: B * L * H * (2 * w.n_tokens - n_recent) * row,
-                    "compact": B * L * H * 4 * w.budget * row}
-    dom = max((names[1], "compact"), key=lambda k: step_us[k])
+    slices = B * L * H
+    if mode & MODE_BITS["tar_adjacent"]:
+        # prev-row walk: metadata only; the adjacent sweep reads V and the past K rows
+        algo_by_step = {"adjacent_sweep": slices * (2 * w.n_tokens - n_recent) * row}
+    else:
+        # recent K rows for the table and every V row; then the past K rows
+        algo_by_step = {"table_van": slices * (w.n_tokens + n_recent) * row,
+                        "tar_sweep": slices * (w.n_tokens - n_recent) * row}
+    algo_by_step["compact"] = slices * 4 * w.budget * row
+    dom = max(algo_by_step, key=lambda k: step_us[k])
     achieved = algo_by_step[dom] / (step_us[dom] * 1e-6) / 1e9
 
     out = {

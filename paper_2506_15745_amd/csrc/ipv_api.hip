@@ -161,15 +161,10 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
                                                                           ws_first(ws, d), tar, van, bps, work);
     return launched();
   }
-  if (do_tar) {
-    constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
-    const int32_t blocks = (int32_t)((d.p + GROUPS - 1) / GROUPS);
-    const size_t lds = (size_t)GROUPS * r * sizeof(int32_t);
-    k_recent_table<T, D><<<dim3((uint32_t)(d.slices * blocks)), dim3(256), lds, st>>>(
-        static_cast<const T*>(K), fr, pa, d.S, n, r, (int32_t)d.p, blocks, ws_table(ws), ws_first(ws, d),
-        err_word(ws), zero, zero_per_slice);
-  }
-  IPV_TRY(between());
+  constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
+  const int32_t blocks = (int32_t)((d.p + GROUPS - 1) / GROUPS);
+  const size_t lds = (size_t)GROUPS * r * sizeof(int32_t);
+  const uint32_t table_real = (uint32_t)(d.slices * blocks);
   using C = SweepCfg<T, D>;
   const int32_t col_blocks = (int32_t)((d.p + C::GROUPS - 1) / C::GROUPS);
   const int32_t frame_blocks = (int32_t)(((n + d.p - 1) / d.p + C::U - 1) / C::U);
@@ -178,10 +173,23 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
   const T* k = static_cast<const T*>(K);
   const T* v = static_cast<const T*>(V);
   int32_t* first = ws_first(ws, d);
-  if (do_tar && do_van)
-    k_score_sweep<T, D, true, true><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first, tar,
-                                                            van, err_word(ws), col_blocks, frame_blocks, work);
-  else if (do_tar)
+  if (do_tar && do_van) {
+    // table and VaN tiles in one launch, then the TaR tiles
+    const uint32_t table_padded = pad8(table_real);
+    k_table_van<T, D><<<dim3(table_padded + pad8(work)), block, lds, st>>>(
+        k, v, fr, pa, d.S, n, r, (int32_t)d.p, blocks, table_padded, table_real, ws_table(ws), first, err_word(ws),
+        zero, zero_per_slice, van, col_blocks, frame_blocks, work);
+    IPV_TRY(between());
+    k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
+                                                             tar, van, err_word(ws), col_blocks, frame_blocks, work);
+    return launched();
+  }
+  if (do_tar)
+    k_recent_table<T, D><<<dim3(table_real), block, lds, st>>>(k, fr, pa, d.S, n, r, (int32_t)d.p, blocks,
+                                                               ws_table(ws), first, err_word(ws), zero,
+                                                               zero_per_slice);
+  IPV_TRY(between());
+  if (do_tar)
     k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
                                                              tar, van, err_word(ws), col_blocks, frame_blocks, work);
   else

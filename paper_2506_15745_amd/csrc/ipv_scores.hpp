@@ -1,5 +1,7 @@
-// Scoring kernels of the compression pass: the recent-key table, the fused
-// TaR + VaN row sweep, and the layer-adaptive VaN pooling.
+// Scoring kernels of the compression pass: the recent-key table, the row
+// sweep (TaR and VaN tiles), and the layer-adaptive VaN pooling. A pass that
+// needs both scores runs the table and the VaN tiles in one launch, then the
+// TaR tiles.
 //
 // TaR (Sec. 3.1, TaR equation) averages cos(K[x], K[y]) over the recent rows y
 // at x's patch position. Cosine is linear in the unit vectors, so
@@ -145,9 +147,27 @@ __device__ __forceinline__ void table_block(const T* __restrict__ K, const int32
   }
 }
 
-// zero (optional): the first block of each slice also zeroes zero_per_slice
-// words at zero + slice * zero_per_slice (the compaction flags of a pass,
-// saving a launch).
+// Table block `tb` of the grid: slice tb / blocks_per_slice, GROUPS patch
+// positions from (tb % blocks_per_slice) * GROUPS. zero (optional): the first
+// block of each slice also zeroes zero_per_slice words at
+// zero + slice * zero_per_slice (the compaction flags of a pass, saving a
+// launch). `slot`: GROUPS * r ints of LDS.
+template <typename T, int D>
+__device__ __forceinline__ void table_grid_block(uint32_t tb, const T* __restrict__ K,
+                                                 const int32_t* __restrict__ frame_idx,
+                                                 const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                 int32_t r, int32_t p, int32_t blocks_per_slice,
+                                                 float* __restrict__ table, int32_t* __restrict__ first_recent,
+                                                 uint32_t* err, uint32_t* __restrict__ zero, int32_t zero_per_slice,
+                                                 int32_t* slot) {
+  constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
+  const int64_t slice = tb / blocks_per_slice;
+  const int32_t q0 = (int32_t)(tb % blocks_per_slice) * GROUPS;
+  if (zero && q0 == 0)
+    for (int i = threadIdx.x; i < zero_per_slice; i += 256) zero[slice * zero_per_slice + i] = 0u;
+  table_block<T, D, 256>(K, frame_idx, patch_idx, S, n, r, p, slice, q0, table, first_recent, err, slot);
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, const int32_t* __restrict__ frame_idx,
                                                       const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
@@ -155,16 +175,12 @@ __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, c
                                                       float* __restrict__ table, int32_t* __restrict__ first_recent,
                                                       uint32_t* err, uint32_t* __restrict__ zero,
                                                       int32_t zero_per_slice) {
-  constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
   extern __shared__ int32_t slot[];
-  const int64_t slice = blockIdx.x / blocks_per_slice;
-  const int32_t q0 = (int32_t)(blockIdx.x % blocks_per_slice) * GROUPS;
-  if (zero && q0 == 0)
-    for (int i = threadIdx.x; i < zero_per_slice; i += 256) zero[slice * zero_per_slice + i] = 0u;
-  table_block<T, D, 256>(K, frame_idx, patch_idx, S, n, r, p, slice, q0, table, first_recent, err, slot);
+  table_grid_block<T, D>(blockIdx.x, K, frame_idx, patch_idx, S, n, r, p, blocks_per_slice, table, first_recent, err,
+                         zero, zero_per_slice, slot);
 }
 
-// ---------------------------------------------------------------- fused TaR + VaN sweep
+// ---------------------------------------------------------------- TaR / VaN row sweep
 // Rows are tiled over the (frame, patch) plane of the row space: row x is
 // taken as frame x / p, patch x % p. This covers every row exactly once for
 // any layout, and it is the true position of every row in a cache filled with
@@ -179,7 +195,9 @@ __global__ __launch_bounds__(256) void k_recent_table(const T* __restrict__ K, c
 // never depends on the layout; only the number of m fetches does.
 //
 // Rows at or after first_recent (the start of the recent window, published
-// per slice by the table kernel) are recent: TaR 0 and no K read.
+// per slice by the table kernel) are recent: TaR 0 and no K read. A tile can
+// score both (TAR and VAN) or one of them; the library runs the two halves as
+// separate launches, since the VaN half does not wait for the table.
 template <typename T, int D>
 struct SweepCfg {
   static constexpr int EPL = Lane<T>::EPL;
@@ -332,6 +350,41 @@ __global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, co
   const int32_t rec = TAR ? first_recent[slice] : n;
   sweep_tile<T, D, TAR, VAN>(K, V, patch_idx, S, n, p, table, rec, tar, van, err, slice, f0,
                              (int32_t)(logical % col_blocks), threadIdx.x);
+}
+
+// The recent-key table and the VaN half of the sweep in one launch. The VaN
+// scores need no table, so their tiles can run while the table is built:
+// blocks [0, table_padded) are table blocks (those at or past table_real
+// return at once), dispatched first so that they all start together; the
+// rest are VaN tiles, XCD-mapped like the sweep, which take the slots the
+// table blocks leave and stream V meanwhile. The TaR half of the sweep reads
+// the table, so it is the next launch. table_padded is a multiple of 8, so
+// tile block i + table_padded runs on XCD i % 8.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_table_van(const T* __restrict__ K, const T* __restrict__ V,
+                                                   const int32_t* __restrict__ frame_idx,
+                                                   const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                   int32_t r, int32_t p, int32_t blocks_per_slice,
+                                                   uint32_t table_padded, uint32_t table_real,
+                                                   float* __restrict__ table, int32_t* __restrict__ first_recent,
+                                                   uint32_t* err, uint32_t* __restrict__ zero, int32_t zero_per_slice,
+                                                   float* __restrict__ van, int32_t col_blocks, int32_t frame_blocks,
+                                                   uint32_t n_work) {
+  extern __shared__ int32_t slot[];
+  if (blockIdx.x < table_padded) {
+    if (blockIdx.x < table_real)
+      table_grid_block<T, D>(blockIdx.x, K, frame_idx, patch_idx, S, n, r, p, blocks_per_slice, table, first_recent,
+                             err, zero, zero_per_slice, slot);
+    return;
+  }
+  using C = SweepCfg<T, D>;
+  const uint32_t logical = xcd_logical_id(blockIdx.x - table_padded, gridDim.x - table_padded);
+  if (logical >= n_work) return;
+  const uint32_t tile = logical / col_blocks;
+  const int64_t slice = tile / frame_blocks;
+  const int32_t f0 = (int32_t)(tile % frame_blocks) * C::U;
+  sweep_tile<T, D, false, true>(K, V, patch_idx, S, n, p, table, n, nullptr, van, err, slice, f0,
+                                (int32_t)(logical % col_blocks), threadIdx.x);
 }
 
 // ---------------------------------------------------------------- adaptive pooling
