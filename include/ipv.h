@@ -261,7 +261,11 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
  * counts on entry and receives them on return; passes (host, [B]) receives how
  * many times each stream was compressed. Every step is checked before the
  * first is enqueued (the counts of the whole stretch follow from the counts,
- * rows, mem_cap and budget), so a rejected call enqueues nothing.
+ * rows, mem_cap and budget), so a rejected call enqueues nothing. The
+ * only error that can come after the first launch is IPV_ERR_HIP (the runtime
+ * refused a launch or a copy); n_tokens and passes then describe the frames
+ * enqueued before it. The work of all frames shares tar, van, keep_idx and the
+ * workspace, which hold the last pass's values on return.
  */
 ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                           int32_t* n_tokens, const void* frames_K, const void* frames_V, int32_t n_frames,
