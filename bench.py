@@ -37,8 +37,8 @@ KERNEL_SOURCES = os.path.join(ROOT, "paper_2506_15745_amd", "csrc")
 PEAK_HBM_GBPS = 8000.0
 # the recent-key table runs in one launch with the VaN tiles; the TaR tiles follow
 STEP_NAMES = ("table_van", "tar_sweep", "pool", "select", "compact")
-# with consecutive-frame TaR the first two steps are the prev-row walk and the adjacent sweep
-STEP_NAMES_ADJACENT = ("prev_walk", "adjacent_sweep", "pool", "select", "compact")
+# with consecutive-frame TaR the prev-row walks run with the VaN tiles, then the TaR rows
+STEP_NAMES_ADJACENT = ("prev_van", "adjacent_tar", "pool", "select", "compact")
 MODE_BITS = {"tar_reverse": 1, "van_reverse": 2, "tar_adjacent": 4, "head_shared": 8}
 
 
@@ -325,8 +325,9 @@ def main():
         n_recent = (w.recent_frames - 1) * w.p + w.n_tokens % w.p
     slices = B * L * H
     if mode & MODE_BITS["tar_adjacent"]:
-        # prev-row walk: metadata only; the adjacent sweep reads V and the past K rows
-        algo_by_step = {"adjacent_sweep": slices * (2 * w.n_tokens - n_recent) * row}
+        # every V row beside the walks (which read 8 B of metadata per row); then the past K rows
+        algo_by_step = {"prev_van": slices * w.n_tokens * (row + 8),
+                        "adjacent_tar": slices * (w.n_tokens - n_recent) * row}
     else:
         # recent K rows for the table and every V row; then the past K rows
         algo_by_step = {"table_van": slices * (w.n_tokens + n_recent) * row,

@@ -14,6 +14,7 @@
 #pragma once
 
 #include "ipv_device.hpp"
+#include "ipv_scores.hpp"  // the VaN tiles that share the walk's launch
 
 namespace ipv {
 
@@ -32,25 +33,24 @@ constexpr int kPrevMaxPositions = 8192;
 // (frame, patch) pair, a frame id that decreases, or a patch id outside
 // [0, p) sets an error bit; such metadata gives no defined prev.
 //
-// The chunk metadata is double-buffered; a chunk costs six barriers and no
-// global-memory round trip (the next chunk's loads are in flight meanwhile).
-__global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __restrict__ frame_idx,
-                                                            const int32_t* __restrict__ patch_idx, int64_t S,
-                                                            int32_t n, int32_t r, int32_t p,
-                                                            int32_t* __restrict__ prev,
-                                                            int32_t* __restrict__ first_recent, uint32_t* err,
-                                                            uint32_t* __restrict__ zero, int32_t zero_per_slice) {
+// The chunk's frame ids are double-buffered in LDS; a chunk costs six
+// barriers and no global-memory round trip (the next chunk's loads are in
+// flight meanwhile). One slice's walk is one block of kPrevThreads threads.
+__device__ __forceinline__ void prev_rows_block(int64_t slice, const int32_t* __restrict__ frame_idx,
+                                                const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
+                                                int32_t r, int32_t p, int32_t* __restrict__ prev,
+                                                int32_t* __restrict__ first_recent, uint32_t* err,
+                                                uint32_t* __restrict__ zero, int32_t zero_per_slice) {
   constexpr int NT = kPrevThreads;
   constexpr int BPT = (kPrevMaxPositions + 1 + NT - 1) / NT;  // scan entries per thread
   __shared__ int32_t last[kPrevMaxPositions];
   __shared__ int32_t cnt[kPrevMaxPositions + 1];  // counts, then bucket starts (cnt[p] = rows bucketed)
   __shared__ int32_t bucket[NT];
-  __shared__ int32_t cpa[2][NT], cfr[2][NT];
+  __shared__ int32_t cfr[2][NT];  // chunk frame ids, double-buffered
   __shared__ int32_t scan_tot[NT / kWave];
   // carry: frame id of the previous chunk's last row, and the row its frame starts at
   __shared__ int32_t carry_frame, carry_start;
   const int tid = threadIdx.x;
-  const int64_t slice = blockIdx.x;
   const int64_t base = slice * S;
   if (zero)
     for (int i = tid; i < zero_per_slice; i += NT) zero[slice * zero_per_slice + i] = 0u;
@@ -70,7 +70,6 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
     const bool valid = x < n;
     const int32_t f = nf, q = np;
     const bool inq = valid && q >= 0 && q < p;
-    cpa[b][tid] = q;
     cfr[b][tid] = f;
     __syncthreads();  // (A) chunk metadata visible; counters zero
     {  // the next chunk's metadata is on its way meanwhile
@@ -143,6 +142,44 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
     if (valid && f == fl && (tid > 0 ? cfr[b][tid - 1] != fl : cf != fl)) carry_start = (int32_t)x;
   }
   if (ebits) raise_error(err, ebits);
+}
+
+// grid: one block per slice
+__global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __restrict__ frame_idx,
+                                                            const int32_t* __restrict__ patch_idx, int64_t S,
+                                                            int32_t n, int32_t r, int32_t p,
+                                                            int32_t* __restrict__ prev,
+                                                            int32_t* __restrict__ first_recent, uint32_t* err,
+                                                            uint32_t* __restrict__ zero, int32_t zero_per_slice) {
+  prev_rows_block(blockIdx.x, frame_idx, patch_idx, S, n, r, p, prev, first_recent, err, zero, zero_per_slice);
+}
+
+// The prev-row walk and the VaN tiles of the sweep in one launch (VaN needs
+// no prev rows, so V streams while the walks run): blocks [0, prev_padded)
+// walk one slice each (those at or past `slices` return at once), the rest
+// hold four VaN tiles of 256 threads each, XCD-mapped like the sweep.
+// prev_padded is a multiple of 8, so tile block i + prev_padded runs on XCD
+// i % 8. Both halves fit two blocks per CU (the walk's LDS is under 80 KB).
+template <typename T, int D>
+__global__ __launch_bounds__(kPrevThreads) void k_prev_van(const T* __restrict__ V, const int32_t* __restrict__ frame_idx,
+    const int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t r, int32_t p, int32_t* __restrict__ prev,
+    int32_t* __restrict__ first_recent, uint32_t* err, uint32_t* __restrict__ zero, int32_t zero_per_slice,
+    uint32_t prev_padded, uint32_t slices, float* __restrict__ van, int32_t col_blocks, int32_t frame_blocks,
+    uint32_t n_work) {
+  if (blockIdx.x < prev_padded) {
+    if (blockIdx.x < slices)
+      prev_rows_block(blockIdx.x, frame_idx, patch_idx, S, n, r, p, prev, first_recent, err, zero, zero_per_slice);
+    return;
+  }
+  using C = SweepCfg<T, D>;
+  const uint32_t g = xcd_logical_id(blockIdx.x - prev_padded, gridDim.x - prev_padded);
+  const uint32_t logical = g * 4u + threadIdx.x / 256u;
+  if (logical >= n_work) return;
+  const uint32_t tile = logical / col_blocks;
+  const int64_t slice = tile / frame_blocks;
+  const int32_t f0 = (int32_t)(tile % frame_blocks) * C::U;
+  sweep_tile<T, D, false, true>(V, V, patch_idx, S, n, p, nullptr, n, nullptr, van, err, slice, f0,
+                                (int32_t)(logical % col_blocks), threadIdx.x % 256u);
 }
 
 // Rows are processed in natural order: a block covers GROUPS * U consecutive
