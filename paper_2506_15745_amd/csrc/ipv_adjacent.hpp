@@ -182,17 +182,17 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_van(const T* __restrict__
                                 (int32_t)(logical % col_blocks), threadIdx.x % 256u);
 }
 
-// Rows are processed in natural order: a block covers GROUPS * U consecutive
-// rows, GROUPS rows (contiguous bytes) per step, one lane group of LPR lanes
-// (16 bytes each) per row. K[x] (past rows only) and V[x] loads go out with
-// the prev(x) loads; K[prev(x)] follows once prev(x) is known. Branch-free
-// buffer loads: a lane with nothing to read uses an offset past the end.
-template <typename T, int D, bool VAN>
-__global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K, const T* __restrict__ V,
-                                                        const int32_t* __restrict__ prev, int64_t S, int32_t n,
-                                                        const int32_t* __restrict__ first_recent,
-                                                        float* __restrict__ tar, float* __restrict__ van,
-                                                        int32_t blocks_per_slice, uint32_t n_work) {
+// TaR of the past rows against their prev rows. Rows are processed in
+// natural order: a block covers GROUPS * U consecutive rows, GROUPS rows
+// (contiguous bytes) per step, one lane group of LPR lanes (16 bytes each)
+// per row. K[x] (past rows only) loads go out with the prev(x) loads;
+// K[prev(x)] follows once prev(x) is known. Branch-free buffer loads: a lane
+// with nothing to read uses an offset past the end.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K, const int32_t* __restrict__ prev,
+                                                        int64_t S, int32_t n, const int32_t* __restrict__ first_recent,
+                                                        float* __restrict__ tar, int32_t blocks_per_slice,
+                                                        uint32_t n_work) {
   constexpr int EPL = Lane<T>::EPL, LPR = D / EPL, GROUPS = 256 / LPR, U = 4;
   constexpr uint32_t kSkip = 0xfffffff0u;
   constexpr uint32_t RB = D * (uint32_t)sizeof(T);
@@ -205,10 +205,9 @@ __global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K,
   const int32_t rec = first_recent[slice];
   const uint32_t lo = (uint32_t)lane * EPL * (uint32_t)sizeof(T);
   const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(K + base * D, (uint32_t)S * RB);
-  const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(V + base * D, (uint32_t)S * RB);
   const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(prev + base, (uint32_t)(S * 4));
   int32_t y[U];
-  Raw16 kx[U], ky[U], vx[U];
+  Raw16 kx[U], ky[U];
   auto load = [](const __amdgpu_buffer_rsrc_t& rs, uint32_t off, Raw16& out) {
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
     out.w[0] = v[0];
@@ -223,11 +222,10 @@ __global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K,
     const int32_t yl = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, past ? (uint32_t)x * 4u : kSkip, 0, 0);
     y[u] = past ? yl : -1;
     load(krs, past ? (uint32_t)x * RB + lo : kSkip, kx[u]);
-    if (VAN) load(vrs, x < n ? (uint32_t)x * RB + lo : kSkip, vx[u]);
   }
 #pragma unroll
   for (int u = 0; u < U; ++u) load(krs, y[u] >= 0 ? (uint32_t)y[u] * RB + lo : kSkip, ky[u]);
-  float tsc[U], vsc[U];
+  float tsc[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const float dot = group_sum<LPR>(Lane<T>::dot(kx[u], ky[u]));
@@ -236,14 +234,10 @@ __global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K,
     float sc = (y[u] >= 0 && aa > 0.f && cc > 0.f) ? -(dot * fast_rsqrt(aa) * fast_rsqrt(cc)) : 0.f;
     if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
     tsc[u] = sc;
-    if (VAN) vsc[u] = fast_sqrt(group_sum<LPR>(Lane<T>::sumsq(vx[u])));
   }
   if (lane < U) {
     const int64_t x = r0 + lane * GROUPS + g;
-    if (x < n) {
-      tar[base + x] = lane == 0 ? tsc[0] : lane == 1 ? tsc[1] : lane == 2 ? tsc[2] : tsc[3];
-      if (VAN) van[base + x] = lane == 0 ? vsc[0] : lane == 1 ? vsc[1] : lane == 2 ? vsc[2] : vsc[3];
-    }
+    if (x < n) tar[base + x] = lane == 0 ? tsc[0] : lane == 1 ? tsc[1] : lane == 2 ? tsc[2] : tsc[3];
   }
 }
 

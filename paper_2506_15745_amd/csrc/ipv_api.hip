@@ -144,40 +144,28 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
   const bool do_tar = K != nullptr, do_van = V != nullptr;
   uint32_t* zero = zero_chunks > 0 ? ws_flags(ws, d) : nullptr;
   const int32_t zero_per_slice = (int32_t)(compact_parts(d) * zero_chunks);
-  if (do_tar && do_van && adjacent) {
-    // prev-row walks and VaN tiles in one launch, then the TaR rows
-    using C = SweepCfg<T, D>;
-    const int32_t col_blocks = (int32_t)((d.p + C::GROUPS - 1) / C::GROUPS);
-    const int32_t frame_blocks = (int32_t)(((n + d.p - 1) / d.p + C::U - 1) / C::U);
-    const uint32_t work = (uint32_t)(d.slices * frame_blocks * col_blocks);
-    const uint32_t prev_padded = pad8((uint32_t)d.slices);
-    k_prev_van<T, D><<<dim3(prev_padded + pad8((work + 3) / 4)), dim3(kPrevThreads), 0, st>>>(
-        static_cast<const T*>(V), fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws), zero,
-        zero_per_slice, prev_padded, (uint32_t)d.slices, van, col_blocks, frame_blocks, work);
-    IPV_TRY(between());
-    constexpr int ROWS = 256 / (D / Lane<T>::EPL) * 4;
-    const int32_t bps = (n + ROWS - 1) / ROWS;
-    const uint32_t awork = (uint32_t)(d.slices * bps);
-    const T* k = static_cast<const T*>(K);
-    k_adjacent_sweep<T, D, false><<<dim3(pad8(awork)), dim3(256), 0, st>>>(k, k, ws_prev(ws), d.S, n,
-                                                                        ws_first(ws, d), tar, van, bps, awork);
-    return launched();
-  }
   if (do_tar && adjacent) {
-    k_prev_rows<<<dim3((uint32_t)d.slices), dim3(kPrevThreads), 0, st>>>(
-        fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws), zero, zero_per_slice);
+    if (do_van) {
+      // prev-row walks and VaN tiles in one launch
+      using C = SweepCfg<T, D>;
+      const int32_t col_blocks = (int32_t)((d.p + C::GROUPS - 1) / C::GROUPS);
+      const int32_t frame_blocks = (int32_t)(((n + d.p - 1) / d.p + C::U - 1) / C::U);
+      const uint32_t work = (uint32_t)(d.slices * frame_blocks * col_blocks);
+      const uint32_t prev_padded = pad8((uint32_t)d.slices);
+      k_prev_van<T, D><<<dim3(prev_padded + pad8((work + 3) / 4)), dim3(kPrevThreads), 0, st>>>(
+          static_cast<const T*>(V), fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws),
+          zero, zero_per_slice, prev_padded, (uint32_t)d.slices, van, col_blocks, frame_blocks, work);
+    } else {
+      k_prev_rows<<<dim3((uint32_t)d.slices), dim3(kPrevThreads), 0, st>>>(
+          fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws), zero, zero_per_slice);
+    }
     IPV_TRY(between());
+    // then the TaR rows
     constexpr int ROWS = 256 / (D / Lane<T>::EPL) * 4;
     const int32_t bps = (n + ROWS - 1) / ROWS;
     const uint32_t work = (uint32_t)(d.slices * bps);
-    const T* k = static_cast<const T*>(K);
-    const T* v = static_cast<const T*>(V);
-    if (do_van)
-      k_adjacent_sweep<T, D, true><<<dim3(pad8(work)), dim3(256), 0, st>>>(k, v, ws_prev(ws), d.S, n,
-                                                                         ws_first(ws, d), tar, van, bps, work);
-    else
-      k_adjacent_sweep<T, D, false><<<dim3(pad8(work)), dim3(256), 0, st>>>(k, k, ws_prev(ws), d.S, n,
-                                                                          ws_first(ws, d), tar, van, bps, work);
+    k_adjacent_sweep<T, D><<<dim3(pad8(work)), dim3(256), 0, st>>>(static_cast<const T*>(K), ws_prev(ws), d.S, n,
+                                                                   ws_first(ws, d), tar, bps, work);
     return launched();
   }
   constexpr int GROUPS = 256 / (D / Lane<T>::EPL);
