@@ -132,11 +132,14 @@ uint32_t pad8(uint32_t x) { return (x + 7u) / 8u * 8u; }
 // ------------------------------------------------------------ launchers
 ipv_status no_mark() { return IPV_OK; }
 
-// between(): runs after the recent-key table is enqueued, before the sweep
-// zero_chunks > 0: the table kernel also zeroes the compaction flags for a
+// K == nullptr: VaN only; V == nullptr: TaR only. With both, the first launch
+// builds what TaR needs (the recent-key table, or in the consecutive-frame
+// mode the prev rows) with the VaN tiles beside it, and the second scores
+// TaR. between(): runs after the first launch (the table, the prev rows, or
+// nothing for VaN only), before the sweep that follows.
+// zero_chunks > 0: the first kernel also zeroes the compaction flags for a
 // compaction of zero_chunks chunks per walk that follows in the same pass.
-// adjacent: consecutive-frame TaR (prev-row kernel, then the adjacent sweep,
-// with VaN fused into it when V is given)
+// adjacent: consecutive-frame TaR (IPV_TAR_ADJACENT)
 template <typename T, int D, typename Between>
 ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
                       int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between,
