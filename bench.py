@@ -360,6 +360,7 @@ def main():
         "rows_per_s": round(B * L * H * w.n_tokens / (ms_per_step * 1e-3), 1),
         "algorithmic_bytes": algo,
         "step_us_mean": {k: round(v, 2) for k, v in step_us.items()},
+        "step_GBps": {k: round(v / (step_us[k] * 1e-6) / 1e9, 1) for k, v in algo_by_step.items()},
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
