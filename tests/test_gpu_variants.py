@@ -162,3 +162,19 @@ def test_rows_up_to_the_selection_limit(mode):
     st = synth.fresh_cache(29, 1, 2, n + 3, 64, gh, gw, n, synth.BF16, synth.RhoSpec(0.0, 0.99, 0.3))
     mode_check("n50000", st.K[None], st.V[None], st.frame_idx[None], st.patch_idx[None], n, 20000, 0.5, 6, gh, gw,
                mode)
+
+
+@pytest.mark.parametrize("gh,gw,frames,extra,r,mode,tau", [
+    (64, 128, 3, 0, 1, 0, (0.3, 0.5, 0.7)),        # p = 8192, the largest grid: one pooled frame per round
+    (64, 128, 3, 0, 1, ipv.TAR_ADJACENT, None),     # the prev-row walk's position table full
+    (60, 60, 5, 100, 2, 0, None),                   # p = 3600 with a partial last frame
+    (60, 60, 5, 100, 2, ipv.TAR_ADJACENT | ipv.HEAD_SHARED, None),
+])
+def test_large_patch_grids(gh, gw, frames, extra, r, mode, tau):
+    # hundreds of table blocks and sweep column blocks per slice, more positions than rows per walk chunk
+    p = gh * gw
+    n = frames * p + extra
+    st = synth.fresh_cache(31 + p, 1, 2, n + 4, 64, gh, gw, n, synth.BF16, synth.RhoSpec(0.0, 0.99, 0.3))
+    budget = max(n // 2, min(n, r * p + extra))
+    mode_check("grid%dx%d" % (gh, gw), st.K[None], st.V[None], st.frame_idx[None], st.patch_idx[None], n, budget,
+               0.5, r, gh, gw, mode, cv_tau=tau)
