@@ -259,12 +259,13 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
  * frames_V ([n_frames, B, L, H, rows, D], device, 16-byte aligned), frame id
  * first_frame_id + f and first_patch 0. n_tokens (host, [B]) holds the row
  * counts on entry and receives them on return; passes (host, [B]) receives how
- * many times each stream was compressed. Every step is checked before the
- * first is enqueued (the counts of the whole stretch follow from the counts,
- * rows, mem_cap and budget), so a rejected call enqueues nothing. The
- * only error that can come after the first launch is IPV_ERR_HIP (the runtime
- * refused a launch or a copy); n_tokens and passes then describe the frames
- * enqueued before it. The work of all frames shares tar, van, keep_idx and the
+ * many times each stream was compressed. The frames between two passes go
+ * out as one append launch (the result is that of one append per frame).
+ * Every step is checked before the first is enqueued (the counts of the
+ * whole stretch follow from the counts, rows, mem_cap and budget), so a
+ * rejected call enqueues nothing. The only error that can come after the
+ * first launch is IPV_ERR_HIP (the runtime refused a launch or a copy);
+ * n_tokens and passes then describe the frames enqueued before it. The work of all frames shares tar, van, keep_idx and the
  * workspace, which hold the last pass's values on return.
  */
 ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,

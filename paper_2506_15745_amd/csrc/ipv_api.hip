@@ -299,26 +299,38 @@ ipv_status compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, in
 }
 
 // ------------------------------------------------------------ append
-// Grid-stride copy of the new rows (16 bytes per thread and step) into rows
-// [n, n + rows) of every slice, then the metadata of those rows.
+// `frames` consecutive frames of `rows` rows each into rows
+// [n, n + frames * rows) of every slice. Block row blockIdx.y takes slices
+// blockIdx.y, + gridDim.y, ...; in a slice, a grid-stride loop over the 16-byte
+// pieces of the new rows in destination order (contiguous), then their
+// metadata: frame frame_id + j for the rows of frame j, patch first_patch +
+// the row's place in its frame. Source frame j of slice s starts at byte
+// j * frame_stride + s * rows * RB. The caller keeps frames * rows * RB within
+// the slice's 32-bit byte range (n + frames * rows <= S).
 __global__ __launch_bounds__(256) void k_append(const char* __restrict__ Kn, const char* __restrict__ Vn,
                                                 char* __restrict__ K, char* __restrict__ V,
                                                 int32_t* __restrict__ fr, int32_t* __restrict__ pa, int64_t S,
-                                                int32_t n, int32_t rows, int64_t RB, int32_t frame_id,
-                                                int32_t first_patch, int64_t slices) {
-  const int64_t per_row = RB / 16, per_slice = (int64_t)rows * per_row, total = slices * per_slice;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-    const int64_t slice = i / per_slice, rem = i % per_slice;
-    const int64_t dst = (slice * S + n) * RB + rem * 16;
-    const int64_t src = slice * rows * RB + rem * 16;
-    store16(K + dst, load16(Kn + src));
-    store16(V + dst, load16(Vn + src));
-  }
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < slices * rows; i += stride) {
-    const int64_t slice = i / rows, j = i % rows;
-    fr[slice * S + n + j] = frame_id;
-    pa[slice * S + n + j] = first_patch + (int32_t)j;
+                                                int32_t n, int32_t rows, int32_t frames, int64_t frame_stride,
+                                                int64_t RB, int32_t frame_id, int32_t first_patch, int64_t slices) {
+  const uint32_t per_frame = (uint32_t)rows * (uint32_t)(RB / 16);
+  const uint32_t pieces = (uint32_t)frames * per_frame, meta = (uint32_t)frames * (uint32_t)rows;
+  const uint32_t first = blockIdx.x * blockDim.x + threadIdx.x, step = gridDim.x * blockDim.x;
+  for (int64_t slice = blockIdx.y; slice < slices; slice += gridDim.y) {
+    const char* ks = Kn + slice * rows * RB;
+    const char* vs = Vn + slice * rows * RB;
+    char* kd = K + (slice * S + n) * RB;
+    char* vd = V + (slice * S + n) * RB;
+    for (uint32_t e = first; e < pieces; e += step) {
+      const uint32_t j = e / per_frame;
+      const int64_t src = (int64_t)j * frame_stride + (int64_t)(e - j * per_frame) * 16;
+      store16(kd + (int64_t)e * 16, load16(ks + src));
+      store16(vd + (int64_t)e * 16, load16(vs + src));
+    }
+    for (uint32_t e = first; e < meta; e += step) {
+      const uint32_t j = e / (uint32_t)rows;
+      fr[slice * S + n + e] = frame_id + (int32_t)j;
+      pa[slice * S + n + e] = first_patch + (int32_t)(e - j * (uint32_t)rows);
+    }
   }
 }
 
@@ -410,6 +422,32 @@ ipv_status compress_run(const Dims& d, void* K, void* V, int32_t* fr, int32_t* p
 // per-stream element counts of the arrays
 int64_t kv_bytes_per_stream(const Dims& d) { return d.L * d.H * d.S * d.D * d.elem; }
 int64_t rows_per_stream(const Dims& d) { return d.L * d.H * d.S; }
+
+// Frames [0, frames) of K_new / V_new (frame j at byte j * frame_stride; in
+// a frame the batch's [B, L, H, rows, D] layout) appended to every stream
+// after its n_tokens[b] rows; one launch per run of equal counts (an empty
+// stream appends at row 0 like any other). Arguments checked by the caller.
+ipv_status append_frames(const Dims& d, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                         const int32_t* n_tokens, const void* K_new, const void* V_new, int32_t rows, int32_t frames,
+                         int64_t frame_stride, int32_t frame_id, int32_t first_patch, hipStream_t st) {
+  const int64_t RB = d.D * d.elem;
+  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), nb = d.L * d.H * (int64_t)rows * RB;
+  const int64_t pieces = (int64_t)frames * rows * (RB / 16);
+  for (int64_t b = 0; b < d.B;) {
+    const int32_t n = n_tokens[b];
+    int64_t e = b + 1;
+    while (e < d.B && n_tokens[e] == n) ++e;
+    const int64_t slices = (e - b) * d.L * d.H;
+    const dim3 grid((uint32_t)std::min<int64_t>((pieces + 255) / 256, 256), (uint32_t)std::min<int64_t>(slices, 65535));
+    k_append<<<grid, dim3(256), 0, st>>>(static_cast<const char*>(K_new) + b * nb,
+                                         static_cast<const char*>(V_new) + b * nb, static_cast<char*>(K) + b * kb,
+                                         static_cast<char*>(V) + b * kb, frame_idx + b * rs, patch_idx + b * rs, d.S, n,
+                                         rows, frames, frame_stride, RB, frame_id, first_patch, slices);
+    IPV_TRY(launched());
+    b = e;
+  }
+  return IPV_OK;
+}
 
 }  // namespace
 
@@ -546,24 +584,8 @@ ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_i
   for (int64_t b = 0; b < d.B; ++b)
     if (n_tokens[b] < 0 || (int64_t)n_tokens[b] + rows > d.S) return IPV_ERR_SHAPE;
   if (first_patch < 0 || (int64_t)first_patch + rows > d.p) return IPV_ERR_ARG;
-  const int64_t RB = d.D * d.elem;
-  const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), nb = d.L * d.H * (int64_t)rows * RB;
-  // runs of equal counts; an empty stream appends at row 0 like any other
-  for (int64_t b = 0; b < d.B;) {
-    const int32_t n = n_tokens[b];
-    int64_t e = b + 1;
-    while (e < d.B && n_tokens[e] == n) ++e;
-    const int64_t slices = (e - b) * d.L * d.H;
-    const int64_t chunks = slices * rows * (RB / 16);
-    const uint32_t blocks = (uint32_t)std::min<int64_t>((chunks + 255) / 256, 65536);
-    k_append<<<dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream)>>>(
-        static_cast<const char*>(K_new) + b * nb, static_cast<const char*>(V_new) + b * nb,
-        static_cast<char*>(K) + b * kb, static_cast<char*>(V) + b * kb, frame_idx + b * rs, patch_idx + b * rs, d.S,
-        n, rows, RB, frame_id, first_patch, slices);
-    IPV_TRY(launched());
-    b = e;
-  }
-  return IPV_OK;
+  return append_frames(d, K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, rows, 1, 0, frame_id, first_patch,
+                       static_cast<hipStream_t>(stream));
 }
 
 ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
@@ -638,18 +660,32 @@ ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* fra
     if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
     IPV_TRY(check_ws(d, ws, ws_bytes));
   }
-  const size_t frame_bytes = (size_t)(d.slices * rows * d.D * d.elem);
+  const int64_t frame_bytes = d.slices * rows * d.D * d.elem;
+  const char* fk = static_cast<const char*>(frames_K);
+  const char* fv = static_cast<const char*>(frames_V);
   for (int64_t b = 0; b < d.B; ++b) passes[b] = 0;
   std::vector<int32_t> n_out((size_t)d.B), fired((size_t)d.B);
-  for (int32_t f = 0; f < n_frames; ++f) {
-    IPV_TRY(ipv_ckv_step(shape, K, V, frame_idx, patch_idx, n_tokens, static_cast<const char*>(frames_K) + f * frame_bytes,
-                         static_cast<const char*>(frames_V) + f * frame_bytes, rows, first_frame_id + f, 0, mem_cap,
-                         budget, alpha, recent_frames, mode, cv_tau, tar, van, keep_idx, ws, ws_bytes, n_out.data(),
-                         fired.data(), stream));
-    for (int64_t b = 0; b < d.B; ++b) {
-      n_tokens[b] = n_out[b];
-      passes[b] += fired[b];
+  for (int32_t f = 0; f < n_frames;) {
+    // frames [f, g) bring no stream to the cap: one append launch (per run of
+    // equal counts) for all of them; frame g is a step with its pass
+    int64_t until = INT64_MAX;  // frames until the first stream reaches the cap, that frame included
+    for (int64_t b = 0; b < d.B; ++b) until = std::min<int64_t>(until, (mem_cap - n_tokens[b] + rows - 1) / rows);
+    const int32_t g = (int32_t)std::min<int64_t>(n_frames, f + until - 1);
+    if (g > f) {
+      IPV_TRY(append_frames(d, K, V, frame_idx, patch_idx, n_tokens, fk + f * frame_bytes, fv + f * frame_bytes, rows,
+                            g - f, frame_bytes, first_frame_id + f, 0, static_cast<hipStream_t>(stream)));
+      for (int64_t b = 0; b < d.B; ++b) n_tokens[b] += (g - f) * rows;
     }
+    if (g < n_frames) {
+      IPV_TRY(ipv_ckv_step(shape, K, V, frame_idx, patch_idx, n_tokens, fk + g * frame_bytes, fv + g * frame_bytes, rows,
+                           first_frame_id + g, 0, mem_cap, budget, alpha, recent_frames, mode, cv_tau, tar, van,
+                           keep_idx, ws, ws_bytes, n_out.data(), fired.data(), stream));
+      for (int64_t b = 0; b < d.B; ++b) {
+        n_tokens[b] = n_out[b];
+        passes[b] += fired[b];
+      }
+    }
+    f = g + 1;
   }
   return IPV_OK;
 }
