@@ -190,8 +190,8 @@ def test_compaction_adversarial_patterns(dtype, D):
 
 
 def test_workspace_reused_across_calls_of_different_sizes():
-    # the compaction's tickets, done counter and epoch reset themselves at the end
-    # of every call: one zero-filled workspace serves many calls, of any budget
+    # the pass zeroes the compaction flags it uses in its first kernel: one
+    # workspace serves many calls, of any budget, with no clearing between them
     from paper_2506_15745_amd import ipv
     w = W.Workload(name="reuse", streams=1, layers=3, kv_heads=2, head_dim=128, grid_h=8, grid_w=8,
                    n_tokens=64 * 40, budget=0, recent_frames=3, alphas=(0.5,), dtype=synth.BF16, seeds=(9,),
@@ -213,3 +213,24 @@ def test_workspace_reused_across_calls_of_different_sizes():
                         P.to_host(fd), P.to_host(pd), 0)
         P.check_ascending(keep, w.n_tokens)
         P.oracle_gather_equal(K, V, fr, pa, w.n_tokens, keep, got)
+
+
+def test_nan_scores_are_reported_and_the_pass_stays_well_formed():
+    # bf16 quiet NaNs in one past key and one past value: the NaN value score
+    # is reported in the device error word, the two rows' ranks are
+    # unspecified, and the pass still keeps exactly C ascending rows, the
+    # whole recent window, and compacts the rows it names
+    from paper_2506_15745_amd import ipv
+    w = W.SEVEN_B
+    L = 2
+    K, V, fr, pa = (np.ascontiguousarray(a[:, :L]) for a in cache_of(w))
+    K[0, 1, 2, 500, 7] = 0x7fc0
+    V[0, 0, 3, 1200, 0] = 0x7fc0
+    got = P.gpu_compress(K, V, fr, pa, w.n_tokens, w.budget, 0.5, w.recent_frames, w.grid_h, w.grid_w, None)
+    print("device errors", got.errors, flush=True)
+    assert got.errors & ipv.DEV_NAN
+    assert got.errors & ~(ipv.DEV_NAN) == 0
+    P.check_ascending(got.keep, w.n_tokens)
+    n_recent = w.recent_frames * w.p
+    assert np.all(got.keep[..., -n_recent:] == np.arange(w.n_tokens - n_recent, w.n_tokens, dtype=np.int32))
+    P.oracle_gather_equal(K, V, fr, pa, w.n_tokens, got.keep, got)
