@@ -231,7 +231,7 @@ __global__ __launch_bounds__(256) void k_adjacent_sweep(const T* __restrict__ K,
     const float dot = group_sum<LPR>(Lane<T>::dot(kx[u], ky[u]));
     const float aa = group_sum<LPR>(Lane<T>::sumsq(kx[u]));
     const float cc = group_sum<LPR>(Lane<T>::sumsq(ky[u]));
-    float sc = (y[u] >= 0 && aa > 0.f && cc > 0.f) ? -(dot * fast_rsqrt(aa) * fast_rsqrt(cc)) : 0.f;
+    float sc = (y[u] >= 0 && aa != 0.f && cc != 0.f) ? -(dot * fast_rsqrt(aa) * fast_rsqrt(cc)) : 0.f;  // NaN stays NaN
     if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
     tsc[u] = sc;
   }

@@ -318,7 +318,7 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
       }
       dot = group_sum<LPR>(dot);
       kk = group_sum<LPR>(kk);
-      float sc = kk > 0.f ? -(dot * fast_rsqrt(kk)) : 0.f;
+      float sc = kk != 0.f ? -(dot * fast_rsqrt(kk)) : 0.f;  // a NaN key gives NaN, as in exact arithmetic
       if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
       tsc[u] = past ? sc : 0.f;
     }

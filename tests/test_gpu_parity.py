@@ -216,8 +216,8 @@ def test_workspace_reused_across_calls_of_different_sizes():
 
 
 def test_nan_scores_are_reported_and_the_pass_stays_well_formed():
-    # bf16 quiet NaNs in one past key and one past value: the NaN value score
-    # is reported in the device error word, the two rows' ranks are
+    # bf16 quiet NaNs in one past key and one past value: their NaN scores
+    # are reported in the device error word, the two rows' ranks are
     # unspecified, and the pass still keeps exactly C ascending rows, the
     # whole recent window, and compacts the rows it names
     from paper_2506_15745_amd import ipv
@@ -230,6 +230,8 @@ def test_nan_scores_are_reported_and_the_pass_stays_well_formed():
     print("device errors", got.errors, flush=True)
     assert got.errors & ipv.DEV_NAN
     assert got.errors & ~(ipv.DEV_NAN) == 0
+    # both NaNs reach the scores, as in the oracle's exact arithmetic
+    assert np.isnan(got.tar[0, 1, 2, 500]) and np.isnan(got.van[0, 0, 3, 1200])
     P.check_ascending(got.keep, w.n_tokens)
     n_recent = w.recent_frames * w.p
     assert np.all(got.keep[..., -n_recent:] == np.arange(w.n_tokens - n_recent, w.n_tokens, dtype=np.int32))
