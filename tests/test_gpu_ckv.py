@@ -90,8 +90,10 @@ def test_ckv_loop_with_layer_adaptive_pooling():
     assert passes >= 3
 
 
-@pytest.mark.parametrize("mode", [0, ipv.TAR_ADJACENT | ipv.HEAD_SHARED])
-def test_ckv_stream_equals_step_by_step(mode):
+@pytest.mark.parametrize("mode,dtype,tau", [(0, synth.BF16, None),
+                                            (ipv.TAR_ADJACENT | ipv.HEAD_SHARED, synth.BF16, None),
+                                            (ipv.VAN_REVERSE, synth.F32, (0.3, 0.5, 0.7))])
+def test_ckv_stream_equals_step_by_step(mode, dtype, tau):
     # the library-driven loop against the same loop driven from Python, bit for bit,
     # over three streams that start at different fill levels, in two stretches
     L, H, D, gh, gw = 2, 2, 64, 4, 4
@@ -99,15 +101,17 @@ def test_ckv_stream_equals_step_by_step(mode):
     cap, budget, r, frames = 8 * p, 4 * p + 3, 2, 30
     S = cap + p
     B = 3
-    src = [synth.fresh_cache(500 + b, L, H, frames * p, D, gh, gw, frames * p, synth.BF16, synth.RhoSpec(0.0, 0.95))
+    src = [synth.fresh_cache(500 + b, L, H, frames * p, D, gh, gw, frames * p, dtype, synth.RhoSpec(0.0, 0.95))
            for b in range(B)]
+    kind = "bf16" if dtype == synth.BF16 else "raw"
+    tdt, bits = (torch.bfloat16, torch.int16) if dtype == synth.BF16 else (torch.float32, torch.int32)
     fK = np.ascontiguousarray(np.stack([np.stack([s.K[:, :, f * p:(f + 1) * p] for s in src]) for f in range(frames)]))
     fV = np.ascontiguousarray(np.stack([np.stack([s.V[:, :, f * p:(f + 1) * p] for s in src]) for f in range(frames)]))
-    fKd, fVd = P.to_device(fK, "bf16"), P.to_device(fV, "bf16")
+    fKd, fVd = P.to_device(fK, kind), P.to_device(fV, kind)
     start = [0, 2 * p, 5 * p]
 
     def fresh():
-        K = torch.zeros((B, L, H, S, D), dtype=torch.bfloat16, device="cuda:0")
+        K = torch.zeros((B, L, H, S, D), dtype=tdt, device="cuda:0")
         V = torch.zeros_like(K)
         fr = torch.full((B, L, H, S), -1, dtype=torch.int32, device="cuda:0")
         pa = torch.full_like(fr, -1)
@@ -123,21 +127,21 @@ def test_ckv_stream_equals_step_by_step(mode):
     K1, V1, f1, p1, c1 = fresh()
     n1, passes1 = list(start), [0] * B
     for f in range(frames):
-        n1, fired = ipv.ipv_ckv_step(K1, V1, f1, p1, n1, fKd[f], fVd[f], f, 0, cap, budget, 0.5, r, None, c1.tar,
+        n1, fired = ipv.ipv_ckv_step(K1, V1, f1, p1, n1, fKd[f], fVd[f], f, 0, cap, budget, 0.5, r, tau, c1.tar,
                                      c1.van, c1.keep_idx, c1.ws, gh, gw, mode=mode)
         passes1 = [a + int(x) for a, x in zip(passes1, fired)]
     # the library's loop, in two stretches
     K2, V2, f2, p2, c2 = fresh()
-    n2, pa_ = ipv.ipv_ckv_stream(K2, V2, f2, p2, list(start), fKd[:11], fVd[:11], 0, cap, budget, 0.5, r, None,
+    n2, pa_ = ipv.ipv_ckv_stream(K2, V2, f2, p2, list(start), fKd[:11], fVd[:11], 0, cap, budget, 0.5, r, tau,
                                  c2.tar, c2.van, c2.keep_idx, c2.ws, gh, gw, mode=mode)
-    n2, pb_ = ipv.ipv_ckv_stream(K2, V2, f2, p2, n2, fKd[11:], fVd[11:], 11, cap, budget, 0.5, r, None,
+    n2, pb_ = ipv.ipv_ckv_stream(K2, V2, f2, p2, n2, fKd[11:], fVd[11:], 11, cap, budget, 0.5, r, tau,
                                  c2.tar, c2.van, c2.keep_idx, c2.ws, gh, gw, mode=mode)
     torch.cuda.synchronize()
     assert c1.device_errors() == 0 and c2.device_errors() == 0
     assert n2 == n1 and [a + b for a, b in zip(pa_, pb_)] == passes1 and min(passes1) >= 2
     for b in range(B):
         m = n1[b]
-        assert torch.equal(K1[b, :, :, :m].view(torch.int16), K2[b, :, :, :m].view(torch.int16))
-        assert torch.equal(V1[b, :, :, :m].view(torch.int16), V2[b, :, :, :m].view(torch.int16))
+        assert torch.equal(K1[b, :, :, :m].view(bits), K2[b, :, :, :m].view(bits))
+        assert torch.equal(V1[b, :, :, :m].view(bits), V2[b, :, :, :m].view(bits))
         assert torch.equal(f1[b, :, :, :m], f2[b, :, :, :m]) and torch.equal(p1[b, :, :, :m], p2[b, :, :, :m])
     print("passes per stream %s, final rows %s" % (passes1, n1), flush=True)
