@@ -43,7 +43,7 @@ def draw(seed):
                 alpha=alpha, mode=mode, tau=tau)
 
 
-@pytest.mark.parametrize("seed", range(96))
+@pytest.mark.parametrize("seed", range(256))
 def test_random_configuration(seed):
     c = draw(seed)
     print("draw", seed, c, flush=True)
