@@ -8,7 +8,7 @@ cache, all resident in HBM before the timed region, so nothing is restored
 inside it; a 1 GiB write and read evict the caches before warm-up and before
 timing. Prints one JSON line.
 
-  python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 7b-class-28L]
+  python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload 7b-class-28L]
                   [--mode tar_reverse,van_reverse,tar_adjacent,head_shared]
   python bench.py --workload streaming-16x16 --stream   # the whole frame stream: ipv_ckv_step per frame, then ipv_ckv_stream
 """
@@ -84,24 +84,52 @@ def make_cache(w: W.Workload):
     return st("K"), st("V"), st("frame_idx"), st("patch_idx")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, K, V, fr, pa, alpha, seconds, mode=0):
-    """The CPU oracle on the same workload, on this host's cores."""
+    """The CPU oracle on the same workload, on this host's cores; for the tiny
+    and 7B-class caches also on one thread."""
     import oracle
-    # whole passes on fresh copies of the cache (the pass is in place) until
-    # `seconds` of oracle time have been spent; the copies are not timed
-    times = []
-    Kc, Vc, fc, pc = K.copy(), V.copy(), fr.copy(), pa.copy()
-    while not times or (sum(times) < seconds and len(times) < 1000):
-        for dst, src in ((Kc, K), (Vc, V), (fc, fr), (pc, pa)):
-            np.copyto(dst, src)
-        t = time.perf_counter()
-        oracle.compress_inplace(Kc, Vc, fc, pc, w.n_tokens, w.budget, alpha, w.recent_frames, w.grid_h, w.grid_w,
-                                w.cv_tau, mode)
-        times.append(time.perf_counter() - t)
+
+    def passes(budget_s, max_runs):
+        # whole passes on fresh copies of the cache (the pass is in place) until
+        # budget_s of oracle time have been spent; the copies are not timed
+        times = []
+        Kc, Vc, fc, pc = K.copy(), V.copy(), fr.copy(), pa.copy()
+        while not times or (sum(times) < budget_s and len(times) < max_runs):
+            for dst, src in ((Kc, K), (Vc, V), (fc, fr), (pc, pa)):
+                np.copyto(dst, src)
+            t = time.perf_counter()
+            oracle.compress_inplace(Kc, Vc, fc, pc, w.n_tokens, w.budget, alpha, w.recent_frames, w.grid_h, w.grid_w,
+                                    w.cv_tau, mode)
+            times.append(time.perf_counter() - t)
+        return times
+
+    threads = oracle.max_threads()
+    times = passes(seconds, 1000)
     t = statistics.median(times)
-    return {"value": round(w.algorithmic_bytes() / t / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
-            "kind": "oracle", "latency_us": round(t * 1e6, 1),
-            "sample": "whole %s pass, median of %d runs (%.1f s of oracle time)" % (w.name, len(times), sum(times))}
+    out = {"value": round(w.algorithmic_bytes() / t / 1e9, 3), "unit": "GB/s", "cores": threads,
+           "kind": "oracle", "latency_us": round(t * 1e6, 1), "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+           "sample": "whole %s pass, median of %d runs (%.1f s of oracle time)" % (w.name, len(times), sum(times))}
+    if w.name in (W.TINY.name, W.SEVEN_B.name):
+        oracle.set_threads(1)
+        try:
+            one = passes(3.0, 3)
+        finally:
+            oracle.set_threads(threads)
+        t1 = statistics.median(one)
+        out["single_thread"] = {"value": round(w.algorithmic_bytes() / t1 / 1e9, 3), "unit": "GB/s",
+                                "latency_us": round(t1 * 1e6, 1), "runs": len(one)}
+    return out
 
 
 def kernel_source_hash() -> str:
@@ -204,7 +232,7 @@ def copy_probe():
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=W.SEVEN_B.name)
     ap.add_argument("--alpha", type=float, default=None)

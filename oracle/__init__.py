@@ -73,12 +73,19 @@ def lib():
         for f in (L.ipvo_tar_scores, L.ipvo_van_scores, L.ipvo_select, L.ipvo_compact, L.ipvo_compress):
             f.restype = ctypes.c_int
         L.ipvo_max_threads.restype = ctypes.c_int32
+        L.ipvo_set_threads.argtypes = [i32]
+        L.ipvo_set_threads.restype = None
         _lib = L
     return _lib
 
 
 def max_threads() -> int:
     return int(lib().ipvo_max_threads())
+
+
+def set_threads(threads: int) -> None:
+    """Threads of the oracle's slice loops from now on (results do not depend on it)."""
+    lib().ipvo_set_threads(int(threads))
 
 
 def tar_budget_total(alpha: float, budget: int) -> int:

@@ -94,6 +94,10 @@ static double elem(const ipvo_shape* s, const void* base, int64_t sl, int64_t x,
 
 int32_t ipvo_max_threads(void) { return omp_get_max_threads(); }
 
+/* Threads for the slice loops that follow (the benchmark's single-thread
+ * timing); the arithmetic of each slice does not depend on it. */
+void ipvo_set_threads(int32_t threads) { omp_set_num_threads(threads > 0 ? threads : 1); }
+
 /*
  * Recent window of one slice (Sec. 3.1; Algorithm 1 step (2)): rows whose
  * frame id is one of the r latest, counted from the last valid row's frame.
