@@ -159,7 +159,7 @@ __global__ __launch_bounds__(kPrevThreads) void k_prev_rows(const int32_t* __res
 // walk one slice each (those at or past `slices` return at once), the rest
 // hold four VaN tiles of 256 threads each, XCD-mapped like the sweep.
 // prev_padded is a multiple of 8, so tile block i + prev_padded runs on XCD
-// i % 8. Both halves fit two blocks per CU (the walk's LDS is under 80 KB).
+// i % 8.
 template <typename T, int D>
 __global__ __launch_bounds__(kPrevThreads) void k_prev_van(const T* __restrict__ V, const int32_t* __restrict__ frame_idx,
     const int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t r, int32_t p, int32_t* __restrict__ prev,
