@@ -132,13 +132,41 @@ def cpu_baseline(w, K, V, fr, pa, alpha, seconds, mode=0):
     return out
 
 
+def code_only(src: str) -> str:
+    """C++ source without its comments and with whitespace runs folded: what
+    the compiler sees (string and character literals kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the HIP sources: counter readings are valid only for this code."""
+    """Hash of the HIP sources' code (comments and layout ignored): counter
+    readings are valid only for this code."""
     import hashlib
     h = hashlib.sha256()
     for name in sorted(os.listdir(KERNEL_SOURCES)):
-        with open(os.path.join(KERNEL_SOURCES, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+        if not name.endswith((".hip", ".hpp", ".h")):
+            continue
+        with open(os.path.join(KERNEL_SOURCES, name), encoding="utf-8") as f:
+            h.update(name.encode() + b"\0" + code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 
