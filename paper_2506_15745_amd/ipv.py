@@ -123,6 +123,8 @@ def shape_of(K: torch.Tensor, grid_h: int, grid_w: int) -> Shape:
 def _ptr(t):
     if t is None:
         return None
+    if t.device.type != "cuda":
+        raise IpvError(ERR_ARG, "tensors must be in GPU memory (got %s)" % t.device)
     if not t.is_contiguous():
         raise IpvError(ERR_SHAPE, "tensors must be contiguous")
     return t.data_ptr()

@@ -238,3 +238,11 @@ def test_ckv_stream_checks_every_step_before_launch():
     assert run(n=6272) == ipv.ERR_SHAPE           # already at the cap
     assert run(cap=7000) == ipv.ERR_SHAPE
     assert run(frames=0) == ipv.OK and passes[0] == 0    # nothing to do, nothing launched
+
+
+def test_binding_rejects_host_tensors():
+    # a host tensor would hand the kernels a host address: the binding refuses it
+    import torch
+    with pytest.raises(ipv.IpvError) as e:
+        ipv._ptr(torch.zeros(4))
+    assert e.value.status == ipv.ERR_ARG
