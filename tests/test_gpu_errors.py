@@ -1,0 +1,95 @@
+"""Rejected calls on real device buffers: each returns its documented status
+and leaves every buffer byte for byte as it was (the host checks run before
+anything is enqueued), and the device error word stays clear."""
+import ctypes
+
+import pytest
+import torch
+
+from paper_2506_15745_amd import ipv
+from tests import parity as P
+from tests.test_gpu_parity import cache_of
+from synth import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def buffers():
+    w = W.TINY
+    K, V, fr, pa = cache_of(w)
+    Kd, Vd, fd, pd = P.to_device(K), P.to_device(V), P.to_device(fr), P.to_device(pa)
+    comp = ipv.Compressor(Kd, w.grid_h, w.grid_w, w.budget)
+    # recognisable contents in every output and scratch buffer
+    comp.tar.fill_(-3.5)
+    comp.van.fill_(7.25)
+    comp.keep_idx.fill_(-9)
+    # four frames of 16 rows each, [F, B, L, H, rows, D]
+    B, L, H, S, D = Kd.shape
+    fK = torch.arange(4 * B * L * H * 16 * D, dtype=torch.float32, device="cuda:0").view(4, B, L, H, 16, D)
+    fV = fK + 0.5
+    return w, dict(K=Kd, V=Vd, fr=fd, pa=pd, tar=comp.tar, van=comp.van, keep=comp.keep_idx, ws=comp.ws,
+                   fK=fK, fV=fV)
+
+
+def snapshot(b):
+    return {k: t.clone() for k, t in b.items()}
+
+
+def unchanged(b, snap):
+    torch.cuda.synchronize()
+    return all(torch.equal(b[k].view(torch.uint8), snap[k].view(torch.uint8)) for k in b)
+
+
+def ptr(t, off=0):
+    return ctypes.c_void_p(t.data_ptr() + off)
+
+
+def counts(*v):
+    return (ctypes.c_int32 * len(v))(*v)
+
+
+def compress(w, b, n=None, budget=None, alpha=0.5, r=None, mode=0, tau=None, tar_off=0, ws_bytes=None):
+    s = ipv.shape_of(b["K"], w.grid_h, w.grid_w)
+    t = None if tau is None else (ctypes.c_double * 3)(*tau)
+    return ipv.lib().ipv_compress(ctypes.byref(s), ptr(b["K"]), ptr(b["V"]), ptr(b["fr"]), ptr(b["pa"]),
+                                  counts(w.n_tokens if n is None else n), w.budget if budget is None else budget,
+                                  alpha, w.recent_frames if r is None else r, mode,
+                                  None if t is None else ctypes.addressof(t), ptr(b["tar"], tar_off), ptr(b["van"]),
+                                  ptr(b["keep"]), ptr(b["ws"]), b["ws"].numel() if ws_bytes is None else ws_bytes,
+                                  ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+
+
+@pytest.mark.parametrize("case,kw,status", [
+    ("budget below the recent window", dict(budget=15), ipv.ERR_BUDGET),
+    ("budget above the row count", dict(budget=129), ipv.ERR_BUDGET),
+    ("alpha outside [0, 1]", dict(alpha=1.5), ipv.ERR_ARG),
+    ("unknown mode bit", dict(mode=1 << 7), ipv.ERR_ARG),
+    ("thresholds out of order", dict(tau=(0.7, 0.5, 0.3)), ipv.ERR_ARG),
+    ("no recent frame", dict(r=0), ipv.ERR_ARG),
+    ("row count above the capacity", dict(n=129), ipv.ERR_SHAPE),
+    ("misaligned score buffer", dict(tar_off=4), ipv.ERR_ALIGN),
+    ("workspace too small", dict(ws_bytes=256), ipv.ERR_WORKSPACE),
+])
+def test_rejected_pass_touches_nothing(case, kw, status):
+    w, b = buffers()
+    print("case", case, flush=True)
+    snap = snapshot(b)
+    assert compress(w, b, **kw) == status
+    assert unchanged(b, snap)
+    assert ipv.ipv_read_device_errors(b["ws"]) == 0
+
+
+def test_rejected_stream_driver_touches_nothing():
+    # from 64 rows, the fourth 16-row frame reaches the 112-row cap, and its
+    # pass would need a budget below the 16-row window: the call is rejected
+    # before the first three frames are appended
+    w, b = buffers()
+    s = ipv.shape_of(b["K"], w.grid_h, w.grid_w)
+    snap = snapshot(b)
+    n, passes = counts(64), counts(0)
+    rc = ipv.lib().ipv_ckv_stream(ctypes.byref(s), ptr(b["K"]), ptr(b["V"]), ptr(b["fr"]), ptr(b["pa"]), n,
+                                  ptr(b["fK"]), ptr(b["fV"]), 4, 16, 8, 112, 15, 0.5, 1, 0, None, ptr(b["tar"]),
+                                  ptr(b["van"]), ptr(b["keep"]), ptr(b["ws"]), b["ws"].numel(), passes,
+                                  ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert rc == ipv.ERR_BUDGET and n[0] == 64 and passes[0] == 0
+    assert unchanged(b, snap)
