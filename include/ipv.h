@@ -59,8 +59,9 @@
  * ---------------------------------------------------------------- errors
  * Host-checkable argument errors return a non-zero ipv_status before
  * anything is enqueued and leave every buffer untouched. Problems that only
- * the device can see (metadata breaking the invariants above, a keep index
- * outside [j, n), a NaN score) set bits in the workspace's device error word
+ * the device can see (metadata breaking the invariants above, a recent window
+ * larger than the budget, a keep_idx that is not strictly ascending in [0, n),
+ * a NaN score) set bits in the workspace's device error word
  * (IPV_DEV_*); the kernels stay in bounds, skip the offending rows and carry
  * on. Read the word with ipv_read_device_errors, reset it with
  * ipv_clear_device_errors. IPV_ERR_HIP means a launch failed (a stream error
@@ -82,7 +83,7 @@ typedef enum {
   IPV_ERR_ALIGN = 2,       /* a pointer breaks the alignment rules above */
   IPV_ERR_SHAPE = 3,       /* bad B/L/H/D/S/grid, a row count outside [0, S], or a size the kernels do not cover */
   IPV_ERR_DTYPE = 4,       /* dtype is neither IPV_BF16 nor IPV_F32 */
-  IPV_ERR_BUDGET = 5,      /* budget outside [min(n, r*p), n] */
+  IPV_ERR_BUDGET = 5,      /* budget outside [1, n]; ipv_ckv_step / ipv_ckv_stream: outside [min(n, r*p), n] */
   IPV_ERR_ARG = 6,         /* alpha outside [0, 1], recent_frames < 1, bad cv_tau */
   IPV_ERR_WORKSPACE = 7,   /* workspace missing or smaller than ipv_workspace_bytes */
   IPV_ERR_HIP = 8          /* the HIP runtime reported an error */
@@ -95,11 +96,14 @@ enum {
   IPV_DEV_BAD_PATCH = 1u,      /* patch_idx outside [0, p): the row scored 0 / was left out of pooling */
   IPV_DEV_BAD_FRAMES = 2u,     /* frame ids decrease, a (frame, patch) pair repeats in the window (in any
                                   row with IPV_TAR_ADJACENT), or heads differ with IPV_HEAD_SHARED */
-  IPV_DEV_RECENT_OVER = 4u,    /* recent window larger than the budget: keep_idx set to 0..C-1 */
-  IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n): row j was not moved */
+  IPV_DEV_RECENT_OVER = 4u,    /* recent window |R| larger than the budget: keep_idx set to 0..C-1 (the
+                                  compaction then moves nothing) */
+  IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n) or not above keep_idx[j-1]: the compaction
+                                  chunk (256 rows) holding row j was not moved */
   IPV_DEV_NAN = 16u,           /* a candidate score is NaN: its rank is unspecified */
-  IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired (e.g. a workspace shared by
-                                  overlapping calls); its rows were not moved */
+  IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired or its walk's counters were
+                                  not zero (a workspace shared by overlapping calls); its rows were not
+                                  moved */
 };
 
 /*
@@ -170,7 +174,9 @@ ipv_status ipv_van_scores(const ipv_shape* shape, const void* V, const int32_t* 
  *   T = the b_T past rows with the highest tar, V = the b_V past rows outside T
  *   with the highest van; equal scores go to the lower row index, -0.0 == +0.0.
  *   keep_idx = R u T u V in ascending order.
- * Requires min(n, r*p) <= C <= n and n <= 65536.
+ * Requires 1 <= C <= n and n <= 65536. The window |R| comes from the frame
+ * ids on the device: when |R| > C the slice's keep_idx is 0..C-1 and
+ * IPV_DEV_RECENT_OVER is raised.
  * mode: IPV_TAR_REVERSE / IPV_VAN_REVERSE take a stage's lowest scores (ties
  * still to the lower row index); IPV_HEAD_SHARED selects once per layer.
  */
@@ -180,12 +186,15 @@ ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van
 
 /*
  * In-place compaction (Sec. 3.1; Algorithm 1 step (5)): for j < C, row j of
- * K, V, frame_idx and patch_idx becomes a bit copy of row keep_idx[j]. Needs
- * keep_idx[j] in [j, n) (true for any ascending keep set); rows [C, S) are
- * left unspecified and free for new frames. The caller then sets n_tokens[b] = C
- * for every stream with n_tokens[b] > 0.
+ * K, V, frame_idx and patch_idx becomes a bit copy of row keep_idx[j]. Each
+ * slice's keep_idx must be strictly ascending with entries in [0, n) (so
+ * keep_idx[j] >= j), as ipv_select writes it; a chunk of 256 rows holding an
+ * entry that breaks this is not moved and raises IPV_DEV_BAD_KEEP. Rows
+ * [C, S) are left unspecified and free for new frames. The caller then sets
+ * n_tokens[b] = C for every stream with n_tokens[b] > 0.
  * All chunks of all slices are copied in parallel; a chunk stores only after
- * every earlier chunk that reads its rows has loaded them (flags in ws).
+ * every earlier chunk that reads its rows has loaded them (flags and a ticket
+ * counter per walk in ws, zeroed by the call).
  */
 ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                        const int32_t* n_tokens, const int32_t* keep_idx, int32_t budget, void* ws, size_t ws_bytes,
@@ -240,7 +249,9 @@ ipv_status ipv_append(const ipv_shape* shape, void* K, void* V, int32_t* frame_i
  * alone). n_out[b] and compressed[b] (host arrays of B) receive each stream's
  * row count after the step and whether its pass ran.
  * Needs budget <= mem_cap <= S and n_tokens[b] < mem_cap (the previous step
- * left every stream below the cap). Positions: the cache holds keys before the
+ * left every stream below the cap). A pass that runs needs budget >=
+ * min(len, r * p), the largest window a cache of len rows can hold, since the
+ * loop does not read the device between passes. Positions: the cache holds keys before the
  * rotary position encoding and compaction keeps the order of the kept rows,
  * so after every step row j takes position j at decoding, which stays below
  * mem_cap + rows (appendix, positional-encoding details); no position array
@@ -265,8 +276,11 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
  * whole stretch follow from the counts, rows, mem_cap and budget), so a
  * rejected call enqueues nothing. The only error that can come after the
  * first launch is IPV_ERR_HIP (the runtime refused a launch or a copy);
- * n_tokens and passes then describe the frames enqueued before it. The work of all frames shares tar, van, keep_idx and the
- * workspace, which hold the last pass's values on return.
+ * n_tokens and passes then describe the frames enqueued before it. The work
+ * of all frames shares tar, van, keep_idx and the workspace, which hold the
+ * last pass's values on return. Problems only the device sees (IPV_DEV_* bits)
+ * accumulate in the workspace's error word over all passes of the call and do
+ * not stop it: read the word with ipv_read_device_errors after the call.
  */
 ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                           int32_t* n_tokens, const void* frames_K, const void* frames_V, int32_t n_frames,

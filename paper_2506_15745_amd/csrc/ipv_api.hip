@@ -77,10 +77,19 @@ ipv_status check_recent(const Dims& d, int32_t r) {
   return IPV_OK;
 }
 
-ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
-  const int64_t window = std::min<int64_t>(n, (int64_t)r * d.p);
-  if (budget < window || budget > n || budget < 1) return IPV_ERR_BUDGET;
-  return IPV_OK;
+// A pass keeps budget rows of n: 1 <= budget <= n. Whether the budget also
+// holds the recent window |R| depends on the frame ids, which only the device
+// reads: the selection reports a larger window (IPV_DEV_RECENT_OVER).
+ipv_status check_budget(int32_t n, int32_t budget) {
+  return (budget < 1 || budget > n) ? IPV_ERR_BUDGET : IPV_OK;
+}
+
+// The continual-compression loop runs many passes without reading the device
+// between them, so it asks for a budget that holds any window the cache can
+// have: |R| <= min(n, r * p) (a frame holds each patch position at most once).
+ipv_status check_loop_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
+  IPV_TRY(check_budget(n, budget));
+  return budget < std::min<int64_t>(n, (int64_t)r * d.p) ? IPV_ERR_BUDGET : IPV_OK;
 }
 
 // ------------------------------------------------------------ workspace layout
@@ -90,7 +99,8 @@ ipv_status check_budget(const Dims& d, int32_t n, int32_t budget, int32_t r) {
 //                          prev(x) per row instead (slices * S int32)
 // first  slices            int32 first recent row of each slice
 // pool   B * L             int32 pooling window per (stream, layer)
-// flags  walks * chunks    uint32 per compaction chunk (1 once its rows are loaded)
+// flags  walks * (chunks+1) per compaction walk: a uint32 per chunk (1 once its
+//                          rows are loaded), then the walk's ticket counter
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 int64_t compact_parts(const Dims& d) { return 2 * std::max<int64_t>(1, d.D * d.elem / kCompactColBytes) + 1; }
 int64_t max_chunks(const Dims& d) { return (d.S + kCompactRows - 1) / kCompactRows; }
@@ -102,7 +112,7 @@ size_t first_offset(const Dims& d) { return up256(table_offset() + table_bytes(d
 size_t pool_offset(const Dims& d) { return up256(first_offset(d) + (size_t)d.slices * sizeof(int32_t)); }
 size_t flags_offset(const Dims& d) { return up256(pool_offset(d) + (size_t)(d.B * d.L) * sizeof(int32_t)); }
 size_t ws_total(const Dims& d) {
-  return up256(flags_offset(d) + (size_t)(d.slices * compact_parts(d) * max_chunks(d)) * sizeof(uint32_t));
+  return up256(flags_offset(d) + (size_t)(d.slices * compact_parts(d) * walk_words(max_chunks(d))) * sizeof(uint32_t));
 }
 
 ipv_status check_ws(const Dims& d, const void* ws, size_t ws_bytes) {
@@ -146,7 +156,7 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
                       int64_t zero_chunks, bool adjacent) {
   const bool do_tar = K != nullptr, do_van = V != nullptr;
   uint32_t* zero = zero_chunks > 0 ? ws_flags(ws, d) : nullptr;
-  const int32_t zero_per_slice = (int32_t)(compact_parts(d) * zero_chunks);
+  const int32_t zero_per_slice = (int32_t)(compact_parts(d) * walk_words(zero_chunks));
   if (do_tar && adjacent) {
     if (do_van) {
       // prev-row walks and VaN tiles in one launch
@@ -278,8 +288,10 @@ ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa
   using C = CompactCfg<RB, kCompactThreads, kCompactRows, kCompactColBytes>;
   const uint32_t chunks = (uint32_t)compact_chunks(budget);
   const int64_t total = d.slices * C::PARTS * chunks;
-  if (!flags_zeroed)
-    k_clear_flags<<<dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), total);
+  if (!flags_zeroed) {
+    const int64_t words = d.slices * C::PARTS * walk_words(chunks);
+    k_clear_flags<<<dim3((uint32_t)((words + 255) / 256)), dim3(256), 0, st>>>(ws_flags(ws, d), words);
+  }
   k_compact<RB, kCompactThreads, kCompactRows, kCompactColBytes><<<dim3((uint32_t)total), dim3(kCompactThreads), 0, st>>>(
       static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
       chunks);
@@ -390,11 +402,14 @@ ipv_status check_counts(const Dims& d, const int32_t* n_tokens, F each) {
 
 ipv_status no_check(int32_t) { return IPV_OK; }
 
+// loop: the budget check of the continual-compression loop (check_loop_budget)
 ipv_status check_pass_args(const Dims& d, const int32_t* n_tokens, int32_t budget, double alpha, int32_t r,
-                           const double* cv_tau, uint32_t mode) {
+                           const double* cv_tau, uint32_t mode, bool loop = false) {
   IPV_TRY(check_recent(d, r));
   if (!(alpha >= 0.0 && alpha <= 1.0)) return IPV_ERR_ARG;
-  IPV_TRY(check_counts(d, n_tokens, [&](int32_t n) { return check_budget(d, n, budget, r); }));
+  IPV_TRY(check_counts(d, n_tokens, [&](int32_t n) {
+    return loop ? check_loop_budget(d, n, budget, r) : check_budget(n, budget);
+  }));
   IPV_TRY(check_tau(cv_tau));
   return check_mode(mode);
 }
@@ -611,7 +626,7 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
     // every argument of the pass is checked before the append is enqueued
     if (!tar || !van || !keep_idx || !K || !V || !frame_idx || !patch_idx) return IPV_ERR_NULL;
     if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
-    IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode));
+    IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode, true));
     IPV_TRY(check_ws(d, ws, ws_bytes));
   }
   IPV_TRY(ipv_append(shape, K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, rows, frame_id, first_patch, stream));
@@ -651,7 +666,7 @@ ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* fra
       pass[b] = after[b] >= mem_cap ? after[b] : 0;
       any |= pass[b] > 0;
     }
-    if (any) IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode));
+    if (any) IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode, true));
     any_pass |= any;
     for (int64_t b = 0; b < d.B; ++b) n[b] = pass[b] > 0 ? budget : after[b];
   }
@@ -715,7 +730,7 @@ const char* ipv_status_str(ipv_status s) {
     case IPV_ERR_ALIGN: return "a pointer is not aligned as required";
     case IPV_ERR_SHAPE: return "unsupported or inconsistent shape";
     case IPV_ERR_DTYPE: return "unsupported dtype";
-    case IPV_ERR_BUDGET: return "budget outside [min(n, r*p), n]";
+    case IPV_ERR_BUDGET: return "budget outside [1, n] (continual-compression loop: [min(n, r*p), n])";
     case IPV_ERR_ARG: return "invalid argument (alpha, recent_frames or cv_tau)";
     case IPV_ERR_WORKSPACE: return "workspace missing or too small";
     case IPV_ERR_HIP: return "HIP runtime error";

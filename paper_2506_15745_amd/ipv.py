@@ -130,6 +130,78 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def _expect(what, t, shape, dtype, device, optional=False):
+    """Refuse a companion tensor whose shape, dtype or device does not match
+    the cache: the library only sees pointers, so a smaller buffer would be
+    written past its end."""
+    if t is None:
+        if optional:
+            return
+        raise IpvError(ERR_NULL, "%s is required" % what)
+    if t.dtype != dtype:
+        raise IpvError(ERR_DTYPE, "%s must be %s (got %s)" % (what, dtype, t.dtype))
+    if tuple(t.shape) != tuple(shape):
+        raise IpvError(ERR_SHAPE, "%s must have shape %s (got %s)" % (what, tuple(shape), tuple(t.shape)))
+    if t.device != device:
+        raise IpvError(ERR_ARG, "%s is on %s, the cache on %s" % (what, t.device, device))
+
+
+def _check_meta(K, frame_idx, patch_idx):
+    """frame_idx / patch_idx: int32 [B, L, H, S] beside K [B, L, H, S, D]."""
+    rows = tuple(K.shape[:4])
+    _expect("frame_idx", frame_idx, rows, torch.int32, K.device)
+    _expect("patch_idx", patch_idx, rows, torch.int32, K.device)
+
+
+def _check_scores(ref, device, tar=None, van=None, optional=False):
+    """tar / van: fp32 [B, L, H, S]."""
+    _expect("tar", tar, ref, torch.float32, device, optional)
+    _expect("van", van, ref, torch.float32, device, optional)
+
+
+def _check_keep(keep_idx, rows, budget, device, optional=False):
+    """keep_idx: int32 [B, L, H, budget]."""
+    _expect("keep_idx", keep_idx, tuple(rows[:3]) + (int(budget),), torch.int32, device, optional)
+
+
+def _check_ws(ws, device, optional=False):
+    if ws is None:
+        if optional:
+            return
+        raise IpvError(ERR_WORKSPACE, "a workspace is required")
+    if ws.device != device:
+        raise IpvError(ERR_ARG, "the workspace is on %s, the cache on %s" % (ws.device, device))
+
+
+def _ws_bytes(ws):
+    return 0 if ws is None else ws.numel() * ws.element_size()
+
+
+def _check_cache(K, V, frame_idx, patch_idx):
+    """V like K; the metadata beside them."""
+    _expect("V", V, tuple(K.shape), K.dtype, K.device)
+    _check_meta(K, frame_idx, patch_idx)
+
+
+def _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=False):
+    """Every buffer of a whole pass against the cache K [B, L, H, S, D];
+    optional: the score, keep and workspace buffers may be None (the
+    continual-compression calls need them only when a pass runs)."""
+    _check_cache(K, V, frame_idx, patch_idx)
+    _check_scores(K.shape[:4], K.device, tar, van, optional)
+    _check_keep(keep_idx, K.shape, budget, K.device, optional)
+    _check_ws(ws, K.device, optional)
+
+
+def _check_new_rows(K, K_new, V_new):
+    """K_new / V_new: [B, L, H, rows, D] with the cache's dtype."""
+    if K_new.dtype != K.dtype or V_new.dtype != K.dtype:
+        raise IpvError(ERR_DTYPE, "K_new/V_new must have the cache's dtype")
+    if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
+            or K_new.shape[4] != K.shape[4]:
+        raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
+
+
 def counts(n_tokens, streams: int):
     """Host array of per-stream row counts from an int (every stream) or a sequence."""
     if isinstance(n_tokens, int):
@@ -160,59 +232,77 @@ def alloc_workspace(shape: Shape, device) -> torch.Tensor:
 
 def ipv_tar_scores(K, frame_idx, patch_idx, n_tokens, recent_frames, tar, ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
+    _check_meta(K, frame_idx, patch_idx)
+    _expect("tar", tar, K.shape[:4], torch.float32, K.device)
+    _check_ws(ws, K.device)
     _check(lib().ipv_tar_scores(ctypes.byref(s), _ptr(K), _ptr(frame_idx), _ptr(patch_idx), counts(n_tokens, s.streams),
-                                recent_frames, mode, _ptr(tar), _ptr(ws), ws.numel(), _stream(stream)),
+                                recent_frames, mode, _ptr(tar), _ptr(ws), _ws_bytes(ws), _stream(stream)),
            "ipv_tar_scores")
 
 
 def ipv_van_scores(V, frame_idx, patch_idx, n_tokens, cv_tau, van, pool_size, ws, grid_h, grid_w, stream=None):
     s = shape_of(V, grid_h, grid_w)
+    _check_meta(V, frame_idx, patch_idx)
+    _expect("van", van, V.shape[:4], torch.float32, V.device)
+    _expect("pool_size", pool_size, V.shape[:2], torch.int32, V.device, optional=True)
+    _check_ws(ws, V.device)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_van_scores(ctypes.byref(s), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), counts(n_tokens, s.streams),
                                 None if tau is None else ctypes.addressof(tau), _ptr(van), _ptr(pool_size),
-                                _ptr(ws), ws.numel(), _stream(stream)), "ipv_van_scores")
+                                _ptr(ws), _ws_bytes(ws), _stream(stream)), "ipv_van_scores")
 
 
 def ipv_select(tar, van, frame_idx, n_tokens, budget, alpha, recent_frames, keep_idx, ws, grid_h, grid_w,
                head_dim=128, dtype=BF16, stream=None, mode=0):
     """The select step needs only the slice geometry: (B, L, H, S) from the
     score tensors and the patch grid; head_dim/dtype only size the workspace."""
+    if tar.dim() != 4:
+        raise IpvError(ERR_SHAPE, "tar must be [B, L, H, S]")
     B, L, H, S = tar.shape
     s = Shape(B, L, H, head_dim, S, grid_h, grid_w, dtype)
+    _check_scores(tar.shape, tar.device, tar, van)
+    _expect("frame_idx", frame_idx, tar.shape, torch.int32, tar.device)
+    _check_keep(keep_idx, tar.shape, budget, tar.device)
+    _check_ws(ws, tar.device)
     _check(lib().ipv_select(ctypes.byref(s), _ptr(tar), _ptr(van), _ptr(frame_idx), counts(n_tokens, B), budget,
-                            float(alpha), recent_frames, mode, _ptr(keep_idx), _ptr(ws), ws.numel(),
+                            float(alpha), recent_frames, mode, _ptr(keep_idx), _ptr(ws), _ws_bytes(ws),
                             _stream(stream)),
            "ipv_select")
 
 
 def ipv_compact(K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, grid_h, grid_w, stream=None):
     s = shape_of(K, grid_h, grid_w)
+    _check_cache(K, V, frame_idx, patch_idx)
+    _check_keep(keep_idx, K.shape, budget, K.device)
+    _check_ws(ws, K.device)
     _check(lib().ipv_compact(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
                              counts(n_tokens, s.streams),
-                             _ptr(keep_idx), budget, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)),
+                             _ptr(keep_idx), budget, _ptr(ws), _ws_bytes(ws), _stream(stream)),
            "ipv_compact")
 
 
 def ipv_compress(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van, keep_idx,
                  ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
                               counts(n_tokens, s.streams),
                               budget, float(alpha), recent_frames, mode, None if tau is None else ctypes.addressof(tau),
-                              _ptr(tar), _ptr(van), _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream)),
+                              _ptr(tar), _ptr(van), _ptr(keep_idx), _ptr(ws), _ws_bytes(ws), _stream(stream)),
            "ipv_compress")
 
 
 def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van,
                        keep_idx, ws, grid_h, grid_w, events: Events, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_compress_timed(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
                                     counts(n_tokens, s.streams),
                                     budget, float(alpha), recent_frames, mode,
                                     None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
-                                    _ptr(keep_idx), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(events)),
+                                    _ptr(keep_idx), _ptr(ws), _ws_bytes(ws), _stream(stream), ctypes.byref(events)),
            "ipv_compress_timed")
 
 
@@ -222,9 +312,8 @@ def ipv_append(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, fir
     slice of stream b; returns the new row count(s) (an int for an int
     n_tokens, else a list)."""
     s = shape_of(K, grid_h, grid_w)
-    if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
-            or K_new.shape[4] != K.shape[4] or K_new.dtype != K.dtype:
-        raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
+    _check_cache(K, V, frame_idx, patch_idx)
+    _check_new_rows(K, K_new, V_new)
     rows = K_new.shape[3]
     ns = counts(n_tokens, s.streams)
     _check(lib().ipv_append(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx), ns,
@@ -238,9 +327,9 @@ def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, f
     rows. Returns (row counts, whether each stream's pass ran): ints for an
     int n_tokens (every stream then behaves alike), else lists."""
     s = shape_of(K, grid_h, grid_w)
-    if K_new.shape != V_new.shape or K_new.dim() != 5 or K_new.shape[:3] != K.shape[:3] \
-            or K_new.shape[4] != K.shape[4] or K_new.dtype != K.dtype:
-        raise IpvError(ERR_SHAPE, "K_new/V_new must be [B, L, H, rows, D] like the cache")
+    _check_cache(K, V, frame_idx, patch_idx)
+    _check_new_rows(K, K_new, V_new)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=True)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     n_out, comp = (ctypes.c_int32 * s.streams)(), (ctypes.c_int32 * s.streams)()
     _check(lib().ipv_ckv_step(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
@@ -248,7 +337,7 @@ def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, f
                               _ptr(K_new), _ptr(V_new), K_new.shape[3], frame_id, first_patch, mem_cap, budget,
                               float(alpha), recent_frames, mode, None if tau is None else ctypes.addressof(tau),
                               _ptr(tar),
-                              _ptr(van), _ptr(keep_idx), _ptr(ws), 0 if ws is None else ws.numel(),
+                              _ptr(van), _ptr(keep_idx), _ptr(ws), _ws_bytes(ws),
                               n_out, comp, _stream(stream)), "ipv_ckv_step")
     if isinstance(n_tokens, int):
         return n_out[0], bool(comp[0])
@@ -261,9 +350,13 @@ def ipv_ckv_stream(K, V, frame_idx, patch_idx, n_tokens, frames_K, frames_V, fir
     after another in one library call. Returns (row counts, passes per
     stream): ints for an int n_tokens, else lists."""
     s = shape_of(K, grid_h, grid_w)
+    _check_cache(K, V, frame_idx, patch_idx)
+    if frames_K.dtype != K.dtype or frames_V.dtype != K.dtype:
+        raise IpvError(ERR_DTYPE, "frames_K/V must have the cache's dtype")
     if frames_K.shape != frames_V.shape or frames_K.dim() != 6 or frames_K.shape[1:4] != K.shape[:3] \
-            or frames_K.shape[5] != K.shape[4] or frames_K.dtype != K.dtype:
+            or frames_K.shape[5] != K.shape[4]:
         raise IpvError(ERR_SHAPE, "frames_K/V must be [F, B, L, H, rows, D] like the cache")
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=True)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     ns = counts(n_tokens, s.streams)
     passes = (ctypes.c_int32 * s.streams)()
@@ -271,19 +364,19 @@ def ipv_ckv_stream(K, V, frame_idx, patch_idx, n_tokens, frames_K, frames_V, fir
                                 _ptr(frames_K), _ptr(frames_V), frames_K.shape[0], frames_K.shape[4], first_frame_id,
                                 mem_cap, budget, float(alpha), recent_frames, mode,
                                 None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van), _ptr(keep_idx),
-                                _ptr(ws), 0 if ws is None else ws.numel(), passes, _stream(stream)), "ipv_ckv_stream")
+                                _ptr(ws), _ws_bytes(ws), passes, _stream(stream)), "ipv_ckv_stream")
     if isinstance(n_tokens, int):
         return ns[0], passes[0]
     return list(ns), list(passes)
 
 
 def ipv_clear_device_errors(ws, stream=None):
-    _check(lib().ipv_clear_device_errors(_ptr(ws), ws.numel(), _stream(stream)), "ipv_clear_device_errors")
+    _check(lib().ipv_clear_device_errors(_ptr(ws), _ws_bytes(ws), _stream(stream)), "ipv_clear_device_errors")
 
 
 def ipv_read_device_errors(ws, stream=None) -> int:
     out = ctypes.c_uint32(0)
-    _check(lib().ipv_read_device_errors(_ptr(ws), ws.numel(), _stream(stream), ctypes.byref(out)),
+    _check(lib().ipv_read_device_errors(_ptr(ws), _ws_bytes(ws), _stream(stream), ctypes.byref(out)),
            "ipv_read_device_errors")
     return out.value
 

@@ -87,7 +87,10 @@ def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, w
     (dict(n=-1), ipv.ERR_SHAPE),
     (dict(n=6273), ipv.ERR_SHAPE),                # n > capacity
     (dict(budget=6273), ipv.ERR_BUDGET),          # budget > n
-    (dict(budget=783), ipv.ERR_BUDGET),           # smaller than r * p
+    (dict(budget=0), ipv.ERR_BUDGET),
+    # below r * p passes the host's budget check (only the device sees the
+    # window's size); the zero-byte workspace is what is refused here
+    (dict(budget=783), ipv.ERR_WORKSPACE),
     (dict(alpha=1.5), ipv.ERR_ARG),
     (dict(alpha=float("nan")), ipv.ERR_ARG),
     (dict(r=0), ipv.ERR_ARG),
@@ -136,8 +139,13 @@ def test_entry_points_validate_their_own_arguments():
                             None) == ipv.ERR_ALIGN
     assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 3136, -0.1, 4, 0, FAKE, FAKE, big,
                         None) == ipv.ERR_ARG
-    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 100, 0.5, 4, 0, FAKE, FAKE, big,
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 0, 0.5, 4, 0, FAKE, FAKE, big,
                         None) == ipv.ERR_BUDGET
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 6273, 0.5, 4, 0, FAKE, FAKE, big,
+                        None) == ipv.ERR_BUDGET
+    # a budget below r * p is the device's to judge: here the small workspace is refused
+    assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 100, 0.5, 4, 0, FAKE, FAKE, 8,
+                        None) == ipv.ERR_WORKSPACE
     assert L.ipv_select(ctypes.byref(s), FAKE, FAKE, FAKE, N(6272), 3136, 0.5, 4, 64, FAKE, FAKE, big,
                         None) == ipv.ERR_ARG
     assert L.ipv_compact(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, N(6272), FAKE, 0, None, 0, None) == ipv.ERR_BUDGET
@@ -179,7 +187,7 @@ def test_append_and_ckv_step_validate_before_launch():
     assert step(budget=6300) == ipv.ERR_BUDGET    # budget above the cap
     assert step(tar=None) == ipv.ERR_NULL         # the pass would run: its arguments are checked first
     assert step(wsb=0) == ipv.ERR_WORKSPACE
-    assert step(budget=700) == ipv.ERR_BUDGET     # smaller than the recent window
+    assert step(budget=700) == ipv.ERR_BUDGET     # smaller than any window the loop may meet (r * p = 784)
     assert step(mode=128) == ipv.ERR_ARG          # unknown mode bit
 
 
@@ -246,3 +254,12 @@ def test_binding_rejects_host_tensors():
     with pytest.raises(ipv.IpvError) as e:
         ipv._ptr(torch.zeros(4))
     assert e.value.status == ipv.ERR_ARG
+
+
+def test_budget_from_the_window_up_passes_the_host_checks():
+    # the 72B-class layout: 14x14 grid, r = 8, 36 rows in the last frame, so the
+    # window holds 1408 rows while r * p = 1568; a budget of 1408 is legal and
+    # only the zero-byte workspace is refused here
+    s = shape(layers=80, kv_heads=8, capacity=32768)
+    assert call_compress(s, n=32768, budget=1408, r=8) == ipv.ERR_WORKSPACE
+    assert call_compress(s, n=32768, budget=0, r=8) == ipv.ERR_BUDGET

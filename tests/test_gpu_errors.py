@@ -60,7 +60,7 @@ def compress(w, b, n=None, budget=None, alpha=0.5, r=None, mode=0, tau=None, tar
 
 
 @pytest.mark.parametrize("case,kw,status", [
-    ("budget below the recent window", dict(budget=15), ipv.ERR_BUDGET),
+    ("budget of zero", dict(budget=0), ipv.ERR_BUDGET),
     ("budget above the row count", dict(budget=129), ipv.ERR_BUDGET),
     ("alpha outside [0, 1]", dict(alpha=1.5), ipv.ERR_ARG),
     ("unknown mode bit", dict(mode=1 << 7), ipv.ERR_ARG),
@@ -77,6 +77,20 @@ def test_rejected_pass_touches_nothing(case, kw, status):
     assert compress(w, b, **kw) == status
     assert unchanged(b, snap)
     assert ipv.ipv_read_device_errors(b["ws"]) == 0
+
+
+def test_budget_below_the_window_is_reported_by_the_device():
+    # the host cannot see the window (16 rows here): the selection reports it,
+    # keeps rows 0..C-1, and the compaction then moves nothing
+    w, b = buffers()
+    snap = snapshot(b)
+    assert compress(w, b, budget=15) == ipv.OK
+    torch.cuda.synchronize()
+    assert ipv.ipv_read_device_errors(b["ws"]) == ipv.DEV_RECENT_OVER
+    # keep_idx is [B, L, H, 15] at the front of the 64-wide buffer
+    assert torch.equal(b["keep"].view(-1)[:30].cpu(), torch.arange(15, dtype=torch.int32).repeat(2))
+    for k in ("K", "V", "fr", "pa"):
+        assert torch.equal(b[k].view(torch.uint8), snap[k].view(torch.uint8)), k
 
 
 def test_rejected_stream_driver_touches_nothing():

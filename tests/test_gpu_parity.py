@@ -49,7 +49,8 @@ def full_check(w, K, V, fr, pa, alpha, steps=False, tau=None, n=None, budget=Non
     assert np.array_equal(sel_g.keep_idx, got.keep)
     if steps and tau is not None:
         assert np.array_equal(got.pool_size, pool)
-    print("  max rel err tar %.2e van %.2e, near-threshold rows %d" % (et, ev, near), flush=True)
+    print("  max abs err tar %.2e van %.2e (tolerance used %.3f / %.3f), near-threshold rows %d"
+          % (et["max_abs"], ev["max_abs"], et["max_tol_frac"], ev["max_tol_frac"], near), flush=True)
     return got
 
 

@@ -407,3 +407,30 @@ def test_generator_ar1_lag_correlation():
         assert abs(np.corrcoef(a, b)[0, 1] - st.rho[q]) < 0.05
     z = synth.normals(1, 99, 200000)
     assert abs(z.mean()) < 0.01 and abs(z.std() - 1) < 0.01
+
+
+def test_acceptance_rule_counts():
+    # the comparison rule of oracle/compare.py on a hand-made slice: cut scores
+    # 0.5 (TaR) and 2.0 (VaN); row 3 sits 4e-4 from the TaR cut, so swapping it
+    # for row 4 is a near-threshold flip, and row 9 (VaN score far from its cut)
+    # may move once per TaR flip
+    from oracle import compare
+    o_tar = np.zeros((1, 12))
+    o_van = np.zeros((1, 12))
+    o_tar[0, 3], o_tar[0, 4] = 0.5004, 0.5
+    o_van[0, 9], o_van[0, 8] = 9.0, 2.0
+    o_keep = np.array([[0, 3, 8, 11]])
+    cut_t, cut_v = np.array([0.5]), np.array([2.0])
+    same = compare.keep_stats(o_keep, o_keep, cut_t, cut_v, o_tar, o_van)
+    assert same["slices_differing"] == 0 and same["unexplained_rows"] == 0
+    flip = compare.keep_stats(np.array([[0, 4, 8, 11]]), o_keep, cut_t, cut_v, o_tar, o_van)
+    assert flip["mismatched_rows"] == 2 and flip["near_threshold_rows"] == 2 and flip["unexplained_rows"] == 0
+    # a flip that also displaced a VaN row: one extra row is allowed per TaR flip
+    disp = compare.keep_stats(np.array([[0, 4, 9, 11]]), o_keep, cut_t, cut_v, o_tar, o_van)
+    assert disp["unexplained_rows"] == 0 and disp["mismatched_rows"] == 4
+    # a row far from both cuts with no flip to explain it
+    wrong = compare.keep_stats(np.array([[0, 3, 9, 11]]), o_keep, cut_t, cut_v, o_tar, o_van)
+    assert wrong["unexplained_rows"] == 1 and wrong["worst_slice"] == [0]
+    e = compare.score_errors(np.array([[1.0005, 0.0]], np.float32), np.array([[1.0, 2e-7]]), 2)
+    assert e["max_tol_frac"] <= 1.0 and e["max_abs"] > 4e-4
+    assert compare.score_errors(np.array([[1.0, 3e-6]]), np.array([[1.0, 0.0]]), 2)["max_tol_frac"] > 1.0
