@@ -229,6 +229,26 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
                               void* ws, size_t ws_bytes, void* stream, const ipv_events* events);
 
 /*
+ * ipv_compress for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same pass and the same kernels, with the workspace taken from a 96 MiB
+ * array that the library holds on each GPU it runs on (from the first call on
+ * that GPU until the process ends) instead of a caller buffer. The call itself
+ * allocates nothing. Shapes whose ipv_workspace_bytes exceeds 96 MiB are
+ * refused with IPV_ERR_WORKSPACE (the 7B- and 72B-class caches fit; a batch of
+ * 16 7B-class streams does not). The stream must belong to the current device
+ * (IPV_ERR_ARG otherwise). device_errors (device, 4-byte aligned, may be NULL)
+ * receives the pass's device error word (IPV_DEV_* bits), which the call
+ * clears first. All calls on one GPU share its array: calls that overlap in
+ * time on one GPU (other streams, other host threads) race and must not be
+ * made; calls in sequence on one stream are fine.
+ */
+ipv_status ipv_compress_noalloc(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                                const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                                uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx,
+                                uint32_t* device_errors, void* stream);
+
+/*
  * Append new rows to every slice (Algorithm 1 step (1): the tokens of a new
  * frame, or part of one, join the cache after prefill). Rows
  * [n_tokens[b], n_tokens[b] + rows) of each slice of stream b receive K_new / V_new

@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "../../include/ipv.h"
@@ -558,17 +559,96 @@ ipv_status ipv_compact(const ipv_shape* shape, void* K, void* V, int32_t* frame_
   });
 }
 
+}  // extern "C"
+
+namespace {
+
+// Every host check of a whole pass except the workspace's.
+ipv_status check_compress(const ipv_shape* shape, Dims* d, const void* K, const void* V, const int32_t* frame_idx,
+                          const int32_t* patch_idx, const int32_t* n_tokens, int32_t budget, double alpha,
+                          int32_t recent_frames, uint32_t mode, const double* cv_tau, const float* tar,
+                          const float* van, const int32_t* keep_idx) {
+  IPV_TRY(check_shape(shape, d));
+  if (!K || !V || !frame_idx || !patch_idx || !tar || !van || !keep_idx) return IPV_ERR_NULL;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
+      !aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16))
+    return IPV_ERR_ALIGN;
+  return check_pass_args(*d, n_tokens, budget, alpha, recent_frames, cv_tau, mode);
+}
+
+// ------------------------------------------------------------ allocation-free pass
+// ipv_compress_noalloc's workspace: one array per GPU, allocated with the
+// library's code object when it is loaded on that GPU and held until the
+// process ends. Host code never passes `scratch` itself to a kernel (on the
+// host the name is only a stand-in): it passes the device address that
+// hipGetSymbolAddress returns for the current GPU, looked up on the first
+// call on that GPU and kept per device.
+constexpr size_t kScratchBytes = (size_t)96 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The scratch array of the current device; the stream must belong to it.
+ipv_status scratch_of(hipStream_t st, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return IPV_ERR_HIP;
+  if (st) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(st, &sdev) != hipSuccess) return IPV_ERR_HIP;
+    if ((int)sdev != dev) return IPV_ERR_ARG;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return IPV_ERR_HIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return IPV_OK;
+}
+
+__global__ void k_copy_word(uint32_t* dst, const uint32_t* src) {
+  if (threadIdx.x == 0) *dst = *src;
+}
+
+}  // namespace
+
+extern "C" {
+
+ipv_status ipv_compress_noalloc(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
+                                const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames,
+                                uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx,
+                                uint32_t* device_errors, void* stream) {
+  Dims d;
+  IPV_TRY(check_compress(shape, &d, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, mode,
+                         cv_tau, tar, van, keep_idx));
+  if (ws_total(d) > kScratchBytes) return IPV_ERR_WORKSPACE;
+  if (device_errors && !aligned(device_errors, 4)) return IPV_ERR_ALIGN;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  IPV_TRY(scratch_of(st, &ws));
+  // the error word starts at zero (a kernel, not a memset, so the call can be
+  // captured into a graph); everything else the pass reads it writes first
+  k_fill_i32<<<dim3(1), dim3(64), 0, st>>>(static_cast<int32_t*>(ws), 1, 0);
+  IPV_TRY(launched());
+  IPV_TRY(ipv_compress_timed(shape, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, mode,
+                             cv_tau, tar, van, keep_idx, ws, kScratchBytes, stream, nullptr));
+  if (device_errors) {
+    k_copy_word<<<dim3(1), dim3(64), 0, st>>>(device_errors, err_word(ws));
+    return launched();
+  }
+  return IPV_OK;
+}
+
 ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t* frame_idx, int32_t* patch_idx,
                               const int32_t* n_tokens, int32_t budget, double alpha, int32_t recent_frames,
                               uint32_t mode, const double* cv_tau, float* tar, float* van, int32_t* keep_idx,
                               void* ws, size_t ws_bytes, void* stream, const ipv_events* events) {
   Dims d;
-  IPV_TRY(check_shape(shape, &d));
-  if (!K || !V || !frame_idx || !patch_idx || !tar || !van || !keep_idx) return IPV_ERR_NULL;
-  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
-      !aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16))
-    return IPV_ERR_ALIGN;
-  IPV_TRY(check_pass_args(d, n_tokens, budget, alpha, recent_frames, cv_tau, mode));
+  IPV_TRY(check_compress(shape, &d, K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, mode,
+                         cv_tau, tar, van, keep_idx));
   IPV_TRY(check_ws(d, ws, ws_bytes));
   const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), ks = d.L * d.H * (int64_t)budget;
   return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {

@@ -31,7 +31,7 @@ DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN, DEV_WAIT_
 TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED = 1, 2, 4, 8
 
 EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
-           "ipv_compress", "ipv_compress_timed", "ipv_append", "ipv_ckv_step", "ipv_ckv_stream",
+           "ipv_compress", "ipv_compress_timed", "ipv_compress_noalloc", "ipv_append", "ipv_ckv_step", "ipv_ckv_stream",
            "ipv_clear_device_errors",
            "ipv_read_device_errors", "ipv_status_str")
 
@@ -79,6 +79,7 @@ def lib() -> ctypes.CDLL:
         L.ipv_compress.argtypes = [sp, vp, vp, vp, vp, ns, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp]
         L.ipv_compress_timed.argtypes = [sp, vp, vp, vp, vp, ns, i32, f64, i32, u32, vp, vp, vp, vp, vp, sz, vp,
                                          ctypes.POINTER(Events)]
+        L.ipv_compress_noalloc.argtypes = [sp, vp, vp, vp, vp, ns, i32, f64, i32, u32, vp, vp, vp, vp, vp, vp]
         L.ipv_append.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, vp]
         L.ipv_ckv_step.argtypes = [sp, vp, vp, vp, vp, ns, vp, vp, i32, i32, i32, i32, i32, f64, i32, u32, vp, vp, vp,
                                    vp, vp, sz, ns, ns, vp]
@@ -183,14 +184,16 @@ def _check_cache(K, V, frame_idx, patch_idx):
     _check_meta(K, frame_idx, patch_idx)
 
 
-def _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=False):
+def _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=False,
+                        need_ws=True):
     """Every buffer of a whole pass against the cache K [B, L, H, S, D];
     optional: the score, keep and workspace buffers may be None (the
     continual-compression calls need them only when a pass runs)."""
     _check_cache(K, V, frame_idx, patch_idx)
     _check_scores(K.shape[:4], K.device, tar, van, optional)
     _check_keep(keep_idx, K.shape, budget, K.device, optional)
-    _check_ws(ws, K.device, optional)
+    if need_ws:
+        _check_ws(ws, K.device, optional)
 
 
 def _check_new_rows(K, K_new, V_new):
@@ -304,6 +307,25 @@ def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, rece
                                     None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
                                     _ptr(keep_idx), _ptr(ws), _ws_bytes(ws), _stream(stream), ctypes.byref(events)),
            "ipv_compress_timed")
+
+
+def ipv_compress_noalloc(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van,
+                         keep_idx, grid_h, grid_w, device_errors=None, stream=None, mode=0):
+    """ipv_compress with the library's own per-GPU workspace (no workspace
+    argument, nothing allocated by the call); device_errors: an int32/uint32
+    device tensor of one element that receives the pass's error word, or None."""
+    s = shape_of(K, grid_h, grid_w)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, None, optional=False,
+                        need_ws=False)
+    if device_errors is not None and (device_errors.numel() != 1 or device_errors.element_size() != 4
+                                      or device_errors.device != K.device):
+        raise IpvError(ERR_SHAPE, "device_errors must be one 4-byte element on the cache's device")
+    tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
+    _check(lib().ipv_compress_noalloc(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
+                                      counts(n_tokens, s.streams), budget, float(alpha), recent_frames, mode,
+                                      None if tau is None else ctypes.addressof(tau), _ptr(tar), _ptr(van),
+                                      _ptr(keep_idx), _ptr(device_errors), _stream(stream)),
+           "ipv_compress_noalloc")
 
 
 def ipv_append(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, first_patch, grid_h, grid_w,

@@ -263,3 +263,21 @@ def test_budget_from_the_window_up_passes_the_host_checks():
     s = shape(layers=80, kv_heads=8, capacity=32768)
     assert call_compress(s, n=32768, budget=1408, r=8) == ipv.ERR_WORKSPACE
     assert call_compress(s, n=32768, budget=0, r=8) == ipv.ERR_BUDGET
+
+
+def test_noalloc_refuses_shapes_beyond_its_workspace():
+    # 16 7B-class streams need about 180 MB of workspace, above the 96 MiB array
+    L = ipv.lib()
+    s = shape(streams=16)
+    assert ipv.workspace_bytes(s) > (96 << 20) >= ipv.workspace_bytes(shape(layers=80, kv_heads=8, capacity=32768))
+    ns = N(*([6272] * 16))
+    args = (FAKE, FAKE, FAKE, FAKE, ns, 3136, 0.5, 4, 0, None, FAKE, FAKE, FAKE, None, None)
+    assert L.ipv_compress_noalloc(ctypes.byref(s), *args) == ipv.ERR_WORKSPACE
+    # its other arguments are checked like ipv_compress's, before anything else
+    s1 = shape()
+    assert L.ipv_compress_noalloc(ctypes.byref(s1), FAKE, FAKE, FAKE, FAKE, N(6272), 0, 0.5, 4, 0, None, FAKE, FAKE,
+                                  FAKE, None, None) == ipv.ERR_BUDGET
+    assert L.ipv_compress_noalloc(ctypes.byref(s1), FAKE, None, FAKE, FAKE, N(6272), 3136, 0.5, 4, 0, None, FAKE,
+                                  FAKE, FAKE, None, None) == ipv.ERR_NULL
+    assert L.ipv_compress_noalloc(ctypes.byref(s1), FAKE, FAKE, FAKE, FAKE, N(6272), 3136, 0.5, 4, 0, None, FAKE,
+                                  FAKE, FAKE, FAKE + 2, None) == ipv.ERR_ALIGN
