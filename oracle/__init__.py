@@ -25,8 +25,9 @@ _SRC = os.path.join(_HERE, "ipv_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 OK, ERR_ARG, ERR_META, ERR_BUDGET, ERR_NAN = 0, -1, -2, -3, -4
-# variant bits (the ablation rows of Tab. 5 and the head-shared reading)
-TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED = 1, 2, 4, 8
+# variant bits (the ablation rows of Tab. 5, the head-shared reading, and the
+# Uniform Select baseline of the KV-compression comparison)
+TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED, UNIFORM = 1, 2, 4, 8, 16
 
 
 class OracleError(RuntimeError):
@@ -156,14 +157,20 @@ class Selection:
 def select(tar32, van32, frame_idx, n, budget, alpha, recent_frames, grid_h=1, grid_w=1, mode=0) -> Selection:
     """Keep set from fp32 scores (the precision the decision is taken in). mode:
     TAR_REVERSE / VAN_REVERSE take a stage's lowest scores; HEAD_SHARED ranks
-    the fp32 sum over each layer's heads and gives every head the same rows."""
-    tar32 = _c(tar32, np.float32)
-    van32 = _c(van32, np.float32)
-    B, L, H, S = tar32.shape
+    the fp32 sum over each layer's heads and gives every head the same rows;
+    UNIFORM takes past frames at regular intervals and reads no scores (the
+    score arrays may then be None)."""
+    frame_idx = _c(frame_idx, np.int32)
+    if mode & UNIFORM and tar32 is None:
+        tar32 = van32 = None
+    else:
+        tar32 = _c(tar32, np.float32)
+        van32 = _c(van32, np.float32)
+    B, L, H, S = frame_idx.shape
     s = Shape(B, L, H, 1, S, grid_h, grid_w, 1)
     keep = np.zeros((B, L, H, budget), np.int32)
     info = (SelectInfo * (B * L * H))()
-    _check(lib().ipvo_select(ctypes.byref(s), _ptr(tar32), _ptr(van32), _ptr(_c(frame_idx, np.int32)), n,
+    _check(lib().ipvo_select(ctypes.byref(s), _ptr(tar32), _ptr(van32), _ptr(frame_idx), n,
                              budget, tar_budget_total(alpha, budget), recent_frames, mode, _ptr(keep),
                              ctypes.addressof(info)), "select")
     f = lambda name, dt: np.array([getattr(i, name) for i in info], dt).reshape(B, L, H)

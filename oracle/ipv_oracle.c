@@ -36,6 +36,10 @@
  *                       fp32 sum over the layer's heads of their scores (the
  *                       head-free s(t, i, j) and K[:, I, :] of Sec. 3.1-3.3),
  *                       and every head keeps the same rows
+ *   IPVO_UNIFORM        Uniform Select, the frame-sampling baseline of the
+ *                       KV-compression comparison (appendix, KV cache
+ *                       compression details): past frames at regular
+ *                       intervals, all of their rows, no scores
  *
  * Readings where the paper is silent (documented with the design notes):
  *   - cos(a, b) = 0 when |a||b| = 0; a patch with no key in the recent window
@@ -70,7 +74,14 @@ typedef struct {
 } ipvo_select_info;
 
 enum { IPVO_OK = 0, IPVO_ERR_ARG = -1, IPVO_ERR_META = -2, IPVO_ERR_BUDGET = -3, IPVO_ERR_NAN = -4 };
-enum { IPVO_TAR_REVERSE = 1, IPVO_VAN_REVERSE = 2, IPVO_TAR_ADJACENT = 4, IPVO_HEAD_SHARED = 8, IPVO_MODES = 15 };
+enum {
+  IPVO_TAR_REVERSE = 1,
+  IPVO_VAN_REVERSE = 2,
+  IPVO_TAR_ADJACENT = 4,
+  IPVO_HEAD_SHARED = 8,
+  IPVO_UNIFORM = 16,
+  IPVO_MODES = 31
+};
 
 static int shape_ok(const ipvo_shape* s, int32_t n) {
   if (!s) return 0;
@@ -307,6 +318,46 @@ static int by_score_asc(const void* pa, const void* pb, void* ctx) {
 }
 
 /*
+ * Uniform Select (appendix, KV cache compression details: frames taken at
+ * regular intervals with every token of each taken frame). With the recent
+ * window R kept as in the other modes, the past rows P = [0, n - |R|) hold q
+ * distinct frame ids; number them 0..q-1 in row order. The past budget
+ * b = C - |R| buys k = ceil(b * q / |P|) frames (b in frames of the past's
+ * average size, rounded up), taken at ranks floor(j * q / k), j = 0..k-1
+ * (steps of q / k >= 1 frames from the oldest). The b past rows kept are the
+ * rows of the taken frames in row order (the last one cut short when b is not
+ * a whole number of frames), then, if those frames hold fewer than b rows
+ * (frames that lost rows to earlier passes), the lowest past rows of the
+ * other frames. Writes keep[x] = 1 for the b picks.
+ */
+static void uniform_pick(const int32_t* fr, int32_t n_past, int32_t b, unsigned char* keep) {
+  if (b <= 0) return;
+  /* rank of each past row's frame */
+  int32_t* rank = malloc(sizeof(int32_t) * (size_t)(n_past > 0 ? n_past : 1));
+  int32_t q = 0;
+  for (int32_t x = 0; x < n_past; ++x) {
+    if (x == 0 || fr[x] != fr[x - 1]) ++q;
+    rank[x] = q - 1;
+  }
+  const int64_t k = ((int64_t)b * q + n_past - 1) / n_past;
+  unsigned char* taken = calloc((size_t)q, 1);
+  for (int64_t j = 0; j < k; ++j) taken[(j * q) / k] = 1;
+  int32_t left = b;
+  for (int32_t x = 0; x < n_past && left > 0; ++x)
+    if (taken[rank[x]]) {
+      keep[x] = 1;
+      --left;
+    }
+  for (int32_t x = 0; x < n_past && left > 0; ++x)
+    if (!taken[rank[x]]) {
+      keep[x] = 1;
+      --left;
+    }
+  free(taken);
+  free(rank);
+}
+
+/*
  * One keep set from one pair of fp32 score columns and one frame column.
  * Returns an error bit (0 on success) and fills keep_idx[0..budget) and *inf.
  */
@@ -321,7 +372,16 @@ static int select_one(const float* st, const float* sv, const int32_t* fr, int32
   ipvo_select_info inf = {nr, 0, 0, 0, NAN, NAN};
   if (nr < 0) err |= 2;
   else if (nr > budget) err |= 4;
-  else {
+  else if (mode & IPVO_UNIFORM) {
+    /* the window is a suffix: the past rows are [0, n - nr) */
+    inf.b_van = budget - nr;
+    for (int32_t x = 0; x < n; ++x) keep[x] = rec[x];
+    uniform_pick(fr, n - nr, budget - nr, keep);
+    int32_t j = 0;
+    for (int32_t x = 0; x < n; ++x)
+      if (keep[x]) keep_idx[j++] = x;
+    if (j != budget) err |= 16;
+  } else {
     for (int32_t x = 0; x < n; ++x)
       if (!rec[x] && (isnan(st[x]) || isnan(sv[x]))) err |= 8;
     int32_t bt = tar_budget_total - nr;
@@ -370,23 +430,28 @@ static int select_one(const float* st, const float* sv, const int32_t* fr, int32
  * IPVO_HEAD_SHARED: per (stream, layer), the scores of heads 0..H-1 are added
  * in that order in fp32, every head must hold the same frame ids, and the one
  * keep set (and info) is written for every head.
+ * IPVO_UNIFORM: the past rows come from frames at regular intervals
+ * (uniform_pick); the scores are not read and may be NULL.
  */
 int ipvo_select(const ipvo_shape* s, const float* tar, const float* van, const int32_t* frame_idx, int32_t n,
                 int32_t budget, int32_t tar_budget_total, int32_t recent_frames, uint32_t mode, int32_t* keep_idx,
                 ipvo_select_info* info) {
-  if (!shape_ok(s, n) || !tar || !van || !frame_idx || !keep_idx || recent_frames < 1) return IPVO_ERR_ARG;
+  const int uniform = (mode & IPVO_UNIFORM) != 0;
+  if (!shape_ok(s, n) || (!uniform && (!tar || !van)) || !frame_idx || !keep_idx || recent_frames < 1)
+    return IPVO_ERR_ARG;
   if (mode & ~(uint32_t)IPVO_MODES) return IPVO_ERR_ARG;
   if (budget < 1 || budget > n || tar_budget_total < 0 || tar_budget_total > budget) return IPVO_ERR_BUDGET;
   const int64_t S = s->capacity;
-  const int32_t G = (mode & IPVO_HEAD_SHARED) ? s->kv_heads : 1; /* slices that share one keep set */
+  /* slices that share one keep set; Uniform Select reads frame ids only, the same in every head */
+  const int32_t G = (mode & IPVO_HEAD_SHARED) && !uniform ? s->kv_heads : 1;
   int err = 0;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
   for (int64_t grp = 0; grp < n_slices(s) / G; ++grp) {
     const int64_t sl0 = grp * G;
     ipvo_select_info inf;
     if (G == 1) {
-      err |= select_one(tar + sl0 * S, van + sl0 * S, frame_idx + sl0 * S, n, budget, tar_budget_total,
-                        recent_frames, mode, keep_idx + sl0 * budget, &inf);
+      err |= select_one(uniform ? NULL : tar + sl0 * S, uniform ? NULL : van + sl0 * S, frame_idx + sl0 * S, n,
+                        budget, tar_budget_total, recent_frames, mode, keep_idx + sl0 * budget, &inf);
     } else {
       float* st = malloc(sizeof(float) * (size_t)n);
       float* sv = malloc(sizeof(float) * (size_t)n);
@@ -409,6 +474,14 @@ int ipvo_select(const ipvo_shape* s, const float* tar, const float* van, const i
     }
     if (info)
       for (int32_t h = 0; h < G; ++h) info[sl0 + h] = inf;
+  }
+  if (uniform && (mode & IPVO_HEAD_SHARED)) {
+    /* one keep set per layer: every head must hold the same frame ids (then
+       every head's keep set, computed from them alone, is the same) */
+    const int32_t H = s->kv_heads;
+    for (int64_t sl = 0; sl < n_slices(s); ++sl)
+      for (int32_t x = 0; x < n; ++x)
+        if (frame_idx[sl * S + x] != frame_idx[(sl - sl % H) * S + x]) err |= 2;
   }
   if (err & 2) return IPVO_ERR_META;
   if (err & 4) return IPVO_ERR_BUDGET;
@@ -477,8 +550,11 @@ int ipvo_compress(const ipvo_shape* s, void* K, void* V, int32_t* frame_idx, int
   float* tf = tar_out ? tar_out : calloc((size_t)cells, sizeof(float));
   float* vf = van_out ? van_out : calloc((size_t)cells, sizeof(float));
   int32_t* keep = keep_out ? keep_out : malloc(sizeof(int32_t) * (size_t)(n_slices(s) * budget));
-  int rc = ipvo_tar_scores(s, K, frame_idx, patch_idx, n, recent_frames, mode, tar);
-  if (rc == IPVO_OK) rc = ipvo_van_scores(s, V, frame_idx, patch_idx, n, cv_tau, van, NULL);
+  int rc = IPVO_OK;
+  if (!(mode & IPVO_UNIFORM)) {  /* Uniform Select scores nothing */
+    rc = ipvo_tar_scores(s, K, frame_idx, patch_idx, n, recent_frames, mode, tar);
+    if (rc == IPVO_OK) rc = ipvo_van_scores(s, V, frame_idx, patch_idx, n, cv_tau, van, NULL);
+  }
   if (rc == IPVO_OK) {
     for (int64_t sl = 0; sl < n_slices(s); ++sl)
       for (int32_t x = 0; x < n; ++x) {
