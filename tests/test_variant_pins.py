@@ -226,4 +226,4 @@ def test_unknown_mode_bits_are_rejected():
     z = np.zeros((1, 1, 1, 8), np.float32)
     fr = (np.arange(8, dtype=np.int32) // 2).reshape(1, 1, 1, 8)
     with pytest.raises(oracle.OracleError):
-        oracle.select(z, z, fr, 8, 4, 0.5, 1, mode=16)
+        oracle.select(z, z, fr, 8, 4, 0.5, 1, mode=32)
