@@ -9,7 +9,7 @@ inside it; a 1 GiB write and read evict the caches before warm-up and before
 timing. Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload 7b-class-28L]
-                  [--mode tar_reverse,van_reverse,tar_adjacent,head_shared]
+                  [--mode tar_reverse,van_reverse,tar_adjacent,head_shared,uniform_select]
   python bench.py --workload streaming-16x16 --stream   # the whole frame stream: ipv_ckv_step per frame, then ipv_ckv_stream
 """
 from __future__ import annotations
@@ -39,7 +39,10 @@ PEAK_HBM_GBPS = 8000.0
 STEP_NAMES = ("table_van", "tar_sweep", "pool", "select", "compact")
 # with consecutive-frame TaR the prev-row walks run with the VaN tiles, then the TaR rows
 STEP_NAMES_ADJACENT = ("prev_van", "adjacent_tar", "pool", "select", "compact")
-MODE_BITS = {"tar_reverse": 1, "van_reverse": 2, "tar_adjacent": 4, "head_shared": 8}
+MODE_BITS = {"tar_reverse": 1, "van_reverse": 2, "tar_adjacent": 4, "head_shared": 8, "uniform_select": 16}
+# the oracle's bits for the same variants (the two sides define them separately)
+ORACLE_MODE = {"tar_reverse": "TAR_REVERSE", "van_reverse": "VAN_REVERSE", "tar_adjacent": "TAR_ADJACENT",
+               "head_shared": "HEAD_SHARED", "uniform_select": "UNIFORM"}
 
 
 def parse_mode(text: str) -> int:
@@ -93,6 +96,49 @@ def cpu_model() -> str:
     except OSError:
         pass
     return "unknown"
+
+
+def parity_record(w, K, V, fr, pa, alpha, mode, got):
+    """The oracle's verdict on one GPU pass over the same input bytes (the
+    acceptance rule of oracle/compare.py): largest score errors, keep-set
+    differences split into near-threshold and unexplained rows, and whether
+    the compaction equals the oracle's gather of the GPU's keep set bit for
+    bit. got: host copies of the pass's tar, van, keep_idx and compacted K, V,
+    frame_idx, patch_idx."""
+    import oracle
+    from oracle import compare
+
+    om = sum(getattr(oracle, ORACLE_MODE[k]) for k, b in MODE_BITS.items() if mode & b)
+    n, C, r = w.n_tokens, w.budget, w.recent_frames
+    out = {"slices": int(np.prod(K.shape[:3]))}
+    if mode & MODE_BITS["uniform_select"]:
+        sel = oracle.select(None, None, fr, n, C, alpha, r, mode=om)
+        differ = np.any(got["keep"] != sel.keep_idx, axis=-1)
+        out.update({"keep": "bit-exact (frame ids only)", "slices_differing": int(differ.sum()),
+                    "unexplained_rows": int((got["keep"] != sel.keep_idx).sum())})
+    else:
+        tar64 = oracle.tar_scores(K, fr, pa, n, r, w.grid_h, w.grid_w, mode=om)
+        van64, _ = oracle.van_scores(V, fr, pa, n, w.grid_h, w.grid_w, w.cv_tau)
+        sel = oracle.select(tar64.astype(np.float32), van64.astype(np.float32), fr, n, C, alpha, r, mode=om)
+        et, ev = compare.score_errors(got["tar"], tar64, n), compare.score_errors(got["van"], van64, n)
+        if mode & MODE_BITS["head_shared"]:
+            H = K.shape[2]
+            tar64 = np.repeat(tar64.sum(axis=2, keepdims=True), H, axis=2)
+            van64 = np.repeat(van64.sum(axis=2, keepdims=True), H, axis=2)
+        ks = compare.keep_stats(got["keep"], sel.keep_idx, sel.cut_tar, sel.cut_van, tar64, van64)
+        own = oracle.select(np.ascontiguousarray(got["tar"]), np.ascontiguousarray(got["van"]), fr, n, C, alpha, r,
+                            mode=om)
+        out.update({"tar_max_abs_err": et["max_abs"], "tar_tol_used": round(et["max_tol_frac"], 6),
+                    "van_max_abs_err": ev["max_abs"], "van_tol_used": round(ev["max_tol_frac"], 6),
+                    "slices_differing": ks["slices_differing"], "mismatched_rows": ks["mismatched_rows"],
+                    "near_threshold_rows": ks["near_threshold_rows"], "unexplained_rows": ks["unexplained_rows"],
+                    "keep_equals_oracle_on_gpu_scores": bool(np.array_equal(own.keep_idx, got["keep"]))})
+    Ko, Vo, fo, po = oracle.compact(K, V, fr, pa, n, np.ascontiguousarray(got["keep"]))
+    out["compaction_bit_exact"] = bool(
+        np.array_equal(got["K"][..., :C, :].view(np.uint8), Ko[..., :C, :].view(np.uint8))
+        and np.array_equal(got["V"][..., :C, :].view(np.uint8), Vo[..., :C, :].view(np.uint8))
+        and np.array_equal(got["fr"][..., :C], fo[..., :C]) and np.array_equal(got["pa"][..., :C], po[..., :C]))
+    return out
 
 
 def cpu_baseline(w, K, V, fr, pa, alpha, seconds, mode=0):
@@ -352,13 +398,23 @@ def main():
     evict(1.0)
     for i in range(args.warmup):
         step(i)
+    # an event at every pass boundary of the timed loop: pass j's latency is the
+    # time from its start to the next pass's start (or the end), so the
+    # latencies add up to the loop's device time
+    record = hip.lib.hipEventRecord
+    record.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    bounds = [hip.event() for _ in range(args.steps + 1)]
+    cur = torch.cuda.current_stream().cuda_stream
     evict(2.0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.warmup, args.warmup + args.steps):
+    for j, i in enumerate(range(args.warmup, args.warmup + args.steps)):
+        record(bounds[j], cur)
         step(i)
+    record(bounds[args.steps], cur)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    pass_us = [hip.elapsed_ms(bounds[j], bounds[j + 1]) * 1e3 for j in range(args.steps)]
     # per-kernel breakdown on further replicas, with events between the kernels
     evict(3.0)
     for i in range(args.warmup + args.steps, reps):
@@ -367,12 +423,19 @@ def main():
     errors = comp.device_errors()
 
     timed = range(args.warmup + args.steps, reps)
-    pass_us = [hip.elapsed_ms(events[i][0], events[i][5]) * 1e3 for i in timed]
     step_us = {name: statistics.mean(hip.elapsed_ms(events[i][k], events[i][k + 1]) * 1e3 for i in timed)
                for k, name in enumerate(names)}
+    uniform = bool(mode & MODE_BITS["uniform_select"])
+    if w.cv_tau is None or uniform:
+        del step_us["pool"]  # no pooling kernel runs: its events are back to back
+    if uniform:  # frame ids decide: no score kernels run
+        for k in names[:2]:
+            del step_us[k]
 
     ms_per_step = wall / args.steps * 1e3
     algo = w.algorithmic_bytes()
+    if uniform:  # no scores read: only the compaction's read and write of the kept rows
+        algo = w.streams * w.layers * w.kv_heads * w.head_dim * w.elem_bytes * 4 * w.budget
     value = algo / (ms_per_step * 1e-3) / 1e9
     B, L, H = w.streams, w.layers, w.kv_heads
     row = w.head_dim * w.elem_bytes
@@ -380,7 +443,9 @@ def main():
     if w.n_tokens % w.p:
         n_recent = (w.recent_frames - 1) * w.p + w.n_tokens % w.p
     slices = B * L * H
-    if mode & MODE_BITS["tar_adjacent"]:
+    if uniform:
+        algo_by_step = {}
+    elif mode & MODE_BITS["tar_adjacent"]:
         # every V row beside the walks (which read 8 B of metadata per row); then the past K rows
         algo_by_step = {"prev_van": slices * w.n_tokens * (row + 8),
                         "adjacent_tar": slices * (w.n_tokens - n_recent) * row}
@@ -409,8 +474,9 @@ def main():
                    "tokens_per_frame": w.p, "n_tokens": w.n_tokens, "budget": w.budget,
                    "recent_frames": w.recent_frames, "alpha": alpha, "parallelism": "single GPU",
                    **({"mode": args.mode} if mode else {})},
-        "latency_us": {"wall_mean": round(ms_per_step * 1e3, 2), "events_p50": round(pct(pass_us, 0.5), 2),
-                       "events_p99": round(pct(pass_us, 0.99), 2)},
+        "latency_us": {"wall_mean": round(ms_per_step * 1e3, 2), "events_mean": round(statistics.mean(pass_us), 2),
+                       "p50": round(pct(pass_us, 0.5), 2), "p99": round(pct(pass_us, 0.99), 2),
+                       "source": "events at the timed loop's pass boundaries"},
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
         "tokens_per_s": round(B * w.n_tokens / (ms_per_step * 1e-3), 1),
         "rows_per_s": round(B * L * H * w.n_tokens / (ms_per_step * 1e-3), 1),
@@ -425,6 +491,13 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, K, V, fr, pa, alpha, args.cpu_seconds, mode)
+        # the last replica's pass (same input bytes as every pass) against the oracle
+        Kd, Vd, fd, pd = replicas[reps - 1]
+        host = lambda t: (t.view(torch.int16).cpu().numpy().view(np.uint16) if t.dtype == torch.bfloat16
+                          else t.cpu().numpy())
+        got = {"tar": comp.tar.cpu().numpy(), "van": comp.van.cpu().numpy(), "keep": comp.keep_idx.cpu().numpy(),
+               "K": host(Kd), "V": host(Vd), "fr": fd.cpu().numpy(), "pa": pd.cpu().numpy()}
+        out["cpu_baseline"]["parity"] = parity_record(w, K, V, fr, pa, alpha, mode, got)
     print(json.dumps(out), flush=True)
 
 

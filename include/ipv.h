@@ -125,7 +125,18 @@ enum {
      their scores (fp32, heads added in order 0..H-1 starting from +0); every head
      must hold the same frame ids and receives the same keep_idx row. */
   IPV_HEAD_SHARED = 8u,
-  IPV_MODE_ALL = 15u
+  /* Uniform Select, the frame-sampling baseline of the paper's KV-compression
+     comparison (appendix, KV cache compression details: frames at regular
+     intervals, every token of a taken frame). No scores: the recent window is
+     kept, and the past budget b = C - |R| goes to the q past frames (numbered
+     0..q-1 in row order, |P| past rows) at ranks floor(j * q / k),
+     k = ceil(b * q / |P|): their rows in row order up to b, then, if those
+     frames hold fewer than b rows, the lowest other past rows. tar and van are
+     neither read nor written (they may be NULL) and alpha is unused; the
+     other variant bits do not apply, and with IPV_HEAD_SHARED every head must
+     hold the same frame ids (all heads then keep the same rows). */
+  IPV_UNIFORM_SELECT = 16u,
+  IPV_MODE_ALL = 31u
 };
 
 typedef struct {

@@ -67,6 +67,9 @@ ipv_status check_shape(const ipv_shape* s, Dims* d) {
 
 ipv_status check_mode(uint32_t mode) { return (mode & ~(uint32_t)IPV_MODE_ALL) ? IPV_ERR_ARG : IPV_OK; }
 
+// Uniform Select decides from frame ids: no score buffers are read or written
+bool scores_needed(uint32_t mode) { return (mode & IPV_UNIFORM_SELECT) == 0; }
+
 ipv_status check_rows(const Dims& d, int32_t n) {
   if (n < 1 || n > d.S || n > kMaxRows) return IPV_ERR_SHAPE;
   return IPV_OK;
@@ -270,9 +273,31 @@ ipv_status run_select(const Dims& d, const float* tar, const float* van, const i
   return launched();
 }
 
+// Uniform Select: one block per slice, or per (stream, layer) with IPV_HEAD_SHARED
+template <int RPT>
+ipv_status run_uniform(const Dims& d, const int32_t* fr, int32_t n, int32_t budget, int32_t r, int32_t* keep,
+                       uint32_t* err, hipStream_t st, uint32_t mode) {
+  const int32_t heads = (mode & IPV_HEAD_SHARED) ? (int32_t)d.H : 1;
+  const dim3 grid((uint32_t)(d.slices / heads));
+  if (d.S % 4 == 0)
+    k_select_uniform<kSelThreads, RPT, true><<<grid, dim3(kSelThreads), 0, st>>>(fr, d.S, n, budget, r, keep, err,
+                                                                                 heads);
+  else
+    k_select_uniform<kSelThreads, RPT, false><<<grid, dim3(kSelThreads), 0, st>>>(fr, d.S, n, budget, r, keep, err,
+                                                                                  heads);
+  return launched();
+}
+
 ipv_status select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
                   int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st, uint32_t mode) {
   const int32_t rpt = (n + kSelThreads - 1) / kSelThreads;
+  if (mode & IPV_UNIFORM_SELECT) {
+    if (rpt <= 4) return run_uniform<4>(d, fr, n, budget, r, keep, err, st, mode);
+    if (rpt <= 8) return run_uniform<8>(d, fr, n, budget, r, keep, err, st, mode);
+    if (rpt <= 16) return run_uniform<16>(d, fr, n, budget, r, keep, err, st, mode);
+    if (rpt <= 32) return run_uniform<32>(d, fr, n, budget, r, keep, err, st, mode);
+    return run_uniform<64>(d, fr, n, budget, r, keep, err, st, mode);
+  }
   if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
@@ -423,15 +448,20 @@ ipv_status compress_run(const Dims& d, void* K, void* V, int32_t* fr, int32_t* p
     if (!events || !events->at[i]) return IPV_OK;
     return hipEventRecord(static_cast<hipEvent_t>(events->at[i]), st) == hipSuccess ? IPV_OK : IPV_ERR_HIP;
   };
+  const bool uniform = (mode & IPV_UNIFORM_SELECT) != 0;  // no scores: frame ids decide
   IPV_TRY(mark(0));
-  IPV_TRY(scores(d, K, V, fr, pa, n, r, tar, van, ws, st, [&]() { return mark(1); }, compact_chunks(budget),
-                 (mode & IPV_TAR_ADJACENT) != 0));
+  if (uniform)
+    IPV_TRY(mark(1));
+  else
+    IPV_TRY(scores(d, K, V, fr, pa, n, r, tar, van, ws, st, [&]() { return mark(1); }, compact_chunks(budget),
+                   (mode & IPV_TAR_ADJACENT) != 0));
   IPV_TRY(mark(2));
-  if (cv_tau) IPV_TRY(pool_d(d, cv_tau, van, fr, pa, n, nullptr, ws, st));
+  if (cv_tau && !uniform) IPV_TRY(pool_d(d, cv_tau, van, fr, pa, n, nullptr, ws, st));
   IPV_TRY(mark(3));
   IPV_TRY(select(d, tar, van, fr, n, budget, floor_share(alpha, budget), r, keep, err_word(ws), st, mode));
   IPV_TRY(mark(4));
-  IPV_TRY(compact(d, K, V, fr, pa, n, keep, budget, ws, st, true));
+  // the score launches zero the compaction's flags; without them the compaction does
+  IPV_TRY(compact(d, K, V, fr, pa, n, keep, budget, ws, st, !uniform));
   return mark(5);
 }
 
@@ -530,13 +560,14 @@ ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van
                       int32_t* keep_idx, void* ws, size_t ws_bytes, void* stream) {
   Dims d;
   IPV_TRY(check_shape(shape, &d));
-  if (!tar || !van || !frame_idx || !keep_idx) return IPV_ERR_NULL;
+  if (!frame_idx || !keep_idx || (scores_needed(mode) && (!tar || !van))) return IPV_ERR_NULL;
   if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(frame_idx, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
   IPV_TRY(check_pass_args(d, n_tokens, budget, alpha, recent_frames, nullptr, mode));
   IPV_TRY(check_ws(d, ws, ws_bytes));
   const int64_t rs = rows_per_stream(d), ks = d.L * d.H * (int64_t)budget;
   return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {
-    return select(s, tar + b0 * rs, van + b0 * rs, frame_idx + b0 * rs, n, budget, floor_share(alpha, budget),
+    return select(s, at_stream(tar, b0, rs), at_stream(van, b0, rs), frame_idx + b0 * rs, n, budget,
+                  floor_share(alpha, budget),
                   recent_frames, keep_idx + b0 * ks, err_word(ws), static_cast<hipStream_t>(stream), mode);
   });
 }
@@ -569,7 +600,8 @@ ipv_status check_compress(const ipv_shape* shape, Dims* d, const void* K, const 
                           int32_t recent_frames, uint32_t mode, const double* cv_tau, const float* tar,
                           const float* van, const int32_t* keep_idx) {
   IPV_TRY(check_shape(shape, d));
-  if (!K || !V || !frame_idx || !patch_idx || !tar || !van || !keep_idx) return IPV_ERR_NULL;
+  if (!K || !V || !frame_idx || !patch_idx || !keep_idx || (scores_needed(mode) && (!tar || !van)))
+    return IPV_ERR_NULL;
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(frame_idx, 16) || !aligned(patch_idx, 16) ||
       !aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16))
     return IPV_ERR_ALIGN;
@@ -653,8 +685,8 @@ ipv_status ipv_compress_timed(const ipv_shape* shape, void* K, void* V, int32_t*
   const int64_t kb = kv_bytes_per_stream(d), rs = rows_per_stream(d), ks = d.L * d.H * (int64_t)budget;
   return for_each_run(d, n_tokens, [&](const Dims& s, int64_t b0, int32_t n) {
     return compress_run(s, static_cast<char*>(K) + b0 * kb, static_cast<char*>(V) + b0 * kb, frame_idx + b0 * rs,
-                        patch_idx + b0 * rs, n, budget, alpha, recent_frames, mode, cv_tau, tar + b0 * rs,
-                        van + b0 * rs, keep_idx + b0 * ks, ws, static_cast<hipStream_t>(stream), events);
+                        patch_idx + b0 * rs, n, budget, alpha, recent_frames, mode, cv_tau, at_stream(tar, b0, rs),
+                        at_stream(van, b0, rs), keep_idx + b0 * ks, ws, static_cast<hipStream_t>(stream), events);
   });
 }
 
@@ -704,7 +736,8 @@ ipv_status ipv_ckv_step(const ipv_shape* shape, void* K, void* V, int32_t* frame
   }
   if (any) {
     // every argument of the pass is checked before the append is enqueued
-    if (!tar || !van || !keep_idx || !K || !V || !frame_idx || !patch_idx) return IPV_ERR_NULL;
+    if (!keep_idx || !K || !V || !frame_idx || !patch_idx || (scores_needed(mode) && (!tar || !van)))
+      return IPV_ERR_NULL;
     if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
     IPV_TRY(check_pass_args(d, pass.data(), budget, alpha, recent_frames, cv_tau, mode, true));
     IPV_TRY(check_ws(d, ws, ws_bytes));
@@ -751,7 +784,7 @@ ipv_status ipv_ckv_stream(const ipv_shape* shape, void* K, void* V, int32_t* fra
     for (int64_t b = 0; b < d.B; ++b) n[b] = pass[b] > 0 ? budget : after[b];
   }
   if (any_pass) {
-    if (!tar || !van || !keep_idx) return IPV_ERR_NULL;
+    if (!keep_idx || (scores_needed(mode) && (!tar || !van))) return IPV_ERR_NULL;
     if (!aligned(tar, 16) || !aligned(van, 16) || !aligned(keep_idx, 16)) return IPV_ERR_ALIGN;
     IPV_TRY(check_ws(d, ws, ws_bytes));
   }

@@ -369,6 +369,124 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
     if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
 }
 
+// ---------------------------------------------------------------- Uniform Select
+// The frame-sampling baseline of the KV-compression comparison (appendix, KV
+// cache compression details: frames at regular intervals, every token of a
+// taken frame), from frame ids alone. The recent window is kept; the past
+// rows [0, |P|) hold q frames, numbered 0..q-1 in row order; the past budget
+// b = C - |R| buys k = ceil(b * q / |P|) frames at ranks floor(j * q / k). A
+// frame of rank i is taken iff some j * q / k lies in [i, i + 1), i.e.
+// ceil(i * k / q) * q < (i + 1) * k. The b past rows kept are the taken
+// frames' rows in row order, then (if those hold fewer than b rows) the
+// lowest other past rows. Two block scans: frame starts give each row its
+// rank, taken rows give each row its place among them; a row's place among
+// the other past rows is its index minus the taken rows before it, since the
+// past is a prefix of the slice.
+__device__ __forceinline__ bool uniform_taken(int64_t rank, int64_t k, int64_t q) {
+  return (rank * k + q - 1) / q * q < (rank + 1) * k;
+}
+
+template <int NT, int RPT, bool VEC>
+__device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
+                                              int32_t budget, int32_t r, int32_t* __restrict__ keep_idx,
+                                              uint32_t* err, int64_t slice, int32_t heads, SelShared<NT>& sh) {
+  constexpr int NW = NT / kWave;
+  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+  const int64_t base = slice * S;
+  const int64_t row0 = (int64_t)tid * RPT;
+  int32_t* keep = keep_idx + slice * budget;
+  auto put = [&](int32_t j, int32_t row) {
+    for (int32_t h = 0; h < heads; ++h) keep[(int64_t)h * budget + j] = row;
+  };
+
+  uint32_t fr[RPT];
+  load_row_run<RPT, VEC>(frame_idx + base, S, row0, fr);
+  const __amdgpu_buffer_rsrc_t frs = buffer_rsrc(frame_idx + base, (uint32_t)(S * 4));
+  const int32_t last = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)(n - 1) * 4u, 0, 0);
+  const int32_t before = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(
+      frs, (uint32_t)max(row0 - 1, (int64_t)0) * 4u, 0, 0);
+  const int64_t thr = (int64_t)last - r + 1;
+  uint64_t valid = 0, recent = 0, start = 0;
+  bool bad = heads > 1 && heads_differ<RPT, VEC>(frame_idx + base, S, heads, row0, n, fr);
+  int32_t prev = before;
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    if (row0 + i < n) {
+      const int32_t f = (int32_t)fr[i];
+      const bool first = row0 + i == 0;
+      valid |= 1ull << i;
+      const bool rec = (int64_t)f >= thr;
+      if (rec) recent |= 1ull << i;
+      if (rec && (first || (int64_t)prev < thr)) sh.first_recent = (int32_t)(row0 + i);
+      if (first || f != prev) start |= 1ull << i;
+      bad |= !first && f < prev;
+      prev = f;
+    }
+  }
+  const bool wbad = __ballot(bad) != 0;
+  if (lane == 0) sh.wave_bad[w] = wbad;
+  __syncthreads();
+  bool any_bad = false;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) any_bad |= sh.wave_bad[i] != 0;
+  const int32_t n_past = sh.first_recent;
+  const int32_t n_recent = n - n_past;
+  if (any_bad || n_recent > budget) {
+    if (tid == 0) raise_error(err, any_bad ? 2u : 4u);
+    for (int32_t j = tid; j < budget; j += NT) put(j, j);
+    return;
+  }
+  const uint64_t past = valid & ~recent;
+  const int32_t b = budget - n_recent;
+  uint64_t pick = 0;
+  if (b > 0) {
+    // each row's frame rank among the past frames
+    int32_t q32;
+    const int32_t rank0 = block_exclusive_scan<NT>(__popcll(start & past), sh.wave_tot[0], &q32);
+    const int64_t q = q32;
+    const int64_t k = ((int64_t)b * q + n_past - 1) / n_past;
+    uint64_t taken = 0;
+    int64_t rank = rank0 - 1;  // the frame this thread's first row continues, if it is no start
+    bool tk = rank >= 0 && uniform_taken(rank, k, q);
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      if (!((past >> i) & 1ull)) continue;
+      if ((start >> i) & 1ull) tk = uniform_taken(++rank, k, q);
+      if (tk) taken |= 1ull << i;
+    }
+    // places among the taken rows, and among the other past rows
+    int32_t total;
+    int32_t tpos = block_exclusive_scan<NT>(__popcll(taken), sh.wave_tot[1], &total);
+    const int32_t fill = b - total;  // other past rows needed (if positive)
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      if (!((past >> i) & 1ull)) continue;
+      if ((taken >> i) & 1ull) {
+        if (tpos < b) pick |= 1ull << i;
+        ++tpos;
+      } else if (row0 + i - tpos < fill) {
+        pick |= 1ull << i;
+      }
+    }
+  }
+  const uint64_t kept = recent | pick;
+  int32_t total;
+  int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh.wave_tot[2], &total);
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+    if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
+}
+
+// grid: one block per group of `heads` consecutive slices (heads > 1: every
+// head must hold the same frame ids and receives the same keep set)
+template <int NT, int RPT, bool VEC>
+__global__ __launch_bounds__(NT) void k_select_uniform(const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
+                                                       int32_t budget, int32_t r, int32_t* __restrict__ keep_idx,
+                                                       uint32_t* err, int32_t heads) {
+  __shared__ SelShared<NT> sh;
+  uniform_slice<NT, RPT, VEC>(frame_idx, S, n, budget, r, keep_idx, err, (int64_t)blockIdx.x * heads, heads, sh);
+}
+
 // grid: one block per group of `heads` consecutive slices
 template <int NT, int RPT, bool VEC>
 __global__ __launch_bounds__(NT) void k_select(const float* __restrict__ tar, const float* __restrict__ van,

@@ -27,8 +27,9 @@ LIB_PATH = os.path.join(HERE, "libipv.so")
 OK, ERR_NULL, ERR_ALIGN, ERR_SHAPE, ERR_DTYPE, ERR_BUDGET, ERR_ARG, ERR_WORKSPACE, ERR_HIP = range(9)
 BF16, F32 = 0, 1
 DEV_BAD_PATCH, DEV_BAD_FRAMES, DEV_RECENT_OVER, DEV_BAD_KEEP, DEV_NAN, DEV_WAIT_TIMEOUT = 1, 2, 4, 8, 16, 32
-# `mode` bits: reversed TaR / VaN stages, consecutive-frame TaR, head-shared selection
-TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED = 1, 2, 4, 8
+# `mode` bits: reversed TaR / VaN stages, consecutive-frame TaR, head-shared
+# selection, Uniform Select (frames at regular intervals, no scores)
+TAR_REVERSE, VAN_REVERSE, TAR_ADJACENT, HEAD_SHARED, UNIFORM_SELECT = 1, 2, 4, 8, 16
 
 EXPORTS = ("ipv_workspace_bytes", "ipv_tar_scores", "ipv_van_scores", "ipv_select", "ipv_compact",
            "ipv_compress", "ipv_compress_timed", "ipv_compress_noalloc", "ipv_append", "ipv_ckv_step", "ipv_ckv_stream",
@@ -185,12 +186,12 @@ def _check_cache(K, V, frame_idx, patch_idx):
 
 
 def _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=False,
-                        need_ws=True):
+                        need_ws=True, mode=0):
     """Every buffer of a whole pass against the cache K [B, L, H, S, D];
     optional: the score, keep and workspace buffers may be None (the
     continual-compression calls need them only when a pass runs)."""
     _check_cache(K, V, frame_idx, patch_idx)
-    _check_scores(K.shape[:4], K.device, tar, van, optional)
+    _check_scores(K.shape[:4], K.device, tar, van, optional or bool(mode & UNIFORM_SELECT))
     _check_keep(keep_idx, K.shape, budget, K.device, optional)
     if need_ws:
         _check_ws(ws, K.device, optional)
@@ -257,16 +258,17 @@ def ipv_van_scores(V, frame_idx, patch_idx, n_tokens, cv_tau, van, pool_size, ws
 
 def ipv_select(tar, van, frame_idx, n_tokens, budget, alpha, recent_frames, keep_idx, ws, grid_h, grid_w,
                head_dim=128, dtype=BF16, stream=None, mode=0):
-    """The select step needs only the slice geometry: (B, L, H, S) from the
-    score tensors and the patch grid; head_dim/dtype only size the workspace."""
-    if tar.dim() != 4:
-        raise IpvError(ERR_SHAPE, "tar must be [B, L, H, S]")
-    B, L, H, S = tar.shape
+    """The select step needs only the slice geometry: (B, L, H, S) from
+    frame_idx and the patch grid; head_dim/dtype only size the workspace.
+    With UNIFORM_SELECT in mode, tar and van may be None."""
+    if frame_idx.dim() != 4:
+        raise IpvError(ERR_SHAPE, "frame_idx must be [B, L, H, S]")
+    B, L, H, S = frame_idx.shape
     s = Shape(B, L, H, head_dim, S, grid_h, grid_w, dtype)
-    _check_scores(tar.shape, tar.device, tar, van)
-    _expect("frame_idx", frame_idx, tar.shape, torch.int32, tar.device)
-    _check_keep(keep_idx, tar.shape, budget, tar.device)
-    _check_ws(ws, tar.device)
+    _expect("frame_idx", frame_idx, frame_idx.shape, torch.int32, frame_idx.device)
+    _check_scores(frame_idx.shape, frame_idx.device, tar, van, optional=bool(mode & UNIFORM_SELECT))
+    _check_keep(keep_idx, frame_idx.shape, budget, frame_idx.device)
+    _check_ws(ws, frame_idx.device)
     _check(lib().ipv_select(ctypes.byref(s), _ptr(tar), _ptr(van), _ptr(frame_idx), counts(n_tokens, B), budget,
                             float(alpha), recent_frames, mode, _ptr(keep_idx), _ptr(ws), _ws_bytes(ws),
                             _stream(stream)),
@@ -287,7 +289,7 @@ def ipv_compact(K, V, frame_idx, patch_idx, n_tokens, keep_idx, budget, ws, grid
 def ipv_compress(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van, keep_idx,
                  ws, grid_h, grid_w, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
-    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, mode=mode)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_compress(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
                               counts(n_tokens, s.streams),
@@ -299,7 +301,7 @@ def ipv_compress(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_fra
 def ipv_compress_timed(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, recent_frames, cv_tau, tar, van,
                        keep_idx, ws, grid_h, grid_w, events: Events, stream=None, mode=0):
     s = shape_of(K, grid_h, grid_w)
-    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, mode=mode)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     _check(lib().ipv_compress_timed(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
                                     counts(n_tokens, s.streams),
@@ -315,8 +317,7 @@ def ipv_compress_noalloc(K, V, frame_idx, patch_idx, n_tokens, budget, alpha, re
     argument, nothing allocated by the call); device_errors: an int32/uint32
     device tensor of one element that receives the pass's error word, or None."""
     s = shape_of(K, grid_h, grid_w)
-    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, None, optional=False,
-                        need_ws=False)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, None, need_ws=False, mode=mode)
     if device_errors is not None and (device_errors.numel() != 1 or device_errors.element_size() != 4
                                       or device_errors.device != K.device):
         raise IpvError(ERR_SHAPE, "device_errors must be one 4-byte element on the cache's device")
@@ -351,7 +352,7 @@ def ipv_ckv_step(K, V, frame_idx, patch_idx, n_tokens, K_new, V_new, frame_id, f
     s = shape_of(K, grid_h, grid_w)
     _check_cache(K, V, frame_idx, patch_idx)
     _check_new_rows(K, K_new, V_new)
-    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=True)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=True, mode=mode)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     n_out, comp = (ctypes.c_int32 * s.streams)(), (ctypes.c_int32 * s.streams)()
     _check(lib().ipv_ckv_step(ctypes.byref(s), _ptr(K), _ptr(V), _ptr(frame_idx), _ptr(patch_idx),
@@ -378,7 +379,7 @@ def ipv_ckv_stream(K, V, frame_idx, patch_idx, n_tokens, frames_K, frames_V, fir
     if frames_K.shape != frames_V.shape or frames_K.dim() != 6 or frames_K.shape[1:4] != K.shape[:3] \
             or frames_K.shape[5] != K.shape[4]:
         raise IpvError(ERR_SHAPE, "frames_K/V must be [F, B, L, H, rows, D] like the cache")
-    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=True)
+    _check_pass_buffers(K, V, frame_idx, patch_idx, tar, van, keep_idx, budget, ws, optional=True, mode=mode)
     tau = None if cv_tau is None else (ctypes.c_double * 3)(*cv_tau)
     ns = counts(n_tokens, s.streams)
     passes = (ctypes.c_int32 * s.streams)()

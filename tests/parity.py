@@ -116,13 +116,26 @@ def oracle_gather_equal(K0, V0, fr0, pa0, n, keep, got: GpuPass):
 def oracle_mode(mode: int) -> int:
     """The library's mode bits as the oracle's (the two define them separately)."""
     pairs = ((ipv.TAR_REVERSE, oracle.TAR_REVERSE), (ipv.VAN_REVERSE, oracle.VAN_REVERSE),
-             (ipv.TAR_ADJACENT, oracle.TAR_ADJACENT), (ipv.HEAD_SHARED, oracle.HEAD_SHARED))
+             (ipv.TAR_ADJACENT, oracle.TAR_ADJACENT), (ipv.HEAD_SHARED, oracle.HEAD_SHARED),
+             (ipv.UNIFORM_SELECT, oracle.UNIFORM))
     return sum(o for g, o in pairs if mode & g)
+
+
+def check_uniform_pass(name, K, V, fr, pa, n, budget, r, mode, got: GpuPass):
+    """Uniform Select decides from frame ids alone (integer work): the keep
+    set must equal the oracle's bit for bit, and the compaction its gather."""
+    sel = oracle.select(None, None, fr, n, budget, 0.5, r, mode=oracle_mode(mode))
+    check_ascending(got.keep, n)
+    assert np.array_equal(got.keep, sel.keep_idx), "%s: Uniform Select keep set differs" % name
+    oracle_gather_equal(K, V, fr, pa, n, got.keep, got)
+    return 0
 
 
 def check_pass(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, mode, got: GpuPass, cv_tau=None):
     """Every rule above for one pass in any mode; K, V, fr, pa are the cache
     before the pass. Returns the near-threshold row count."""
+    if mode & ipv.UNIFORM_SELECT:
+        return check_uniform_pass(name, K, V, fr, pa, n, budget, r, mode, got)
     om = oracle_mode(mode)
     tar64 = oracle.tar_scores(K, fr, pa, n, r, gh, gw, mode=om)
     van64, _ = oracle.van_scores(V, fr, pa, n, gh, gw, cv_tau)

@@ -100,7 +100,7 @@ def call_compress(s, n=6272, budget=3136, alpha=0.5, r=4, tau=None, ptrs=None, w
     (dict(ws=None), ipv.ERR_WORKSPACE),
     (dict(ws=FAKE + 16), ipv.ERR_ALIGN),
     (dict(), ipv.ERR_WORKSPACE),                  # ws_bytes = 0
-    (dict(mode=16, wsb=1 << 40), ipv.ERR_ARG),    # unknown mode bit
+    (dict(mode=32, wsb=1 << 40), ipv.ERR_ARG),    # unknown mode bit
     (dict(mode=0xffffffff, wsb=1 << 40), ipv.ERR_ARG),
 ])
 def test_compress_rejects_before_launch(case, status):

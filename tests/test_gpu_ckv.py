@@ -72,6 +72,7 @@ def run_loop(L, H, D, gh, gw, frames, cap, budget, r, alpha, dtype, seed, rho_sp
     # the variants over many passes: gappy old frames, heads kept aligned
     (synth.BF16, 128, 3, 4, 6, 2, 2, ipv.HEAD_SHARED | ipv.TAR_ADJACENT),
     (synth.F32, 64, 2, 5, 8, 3, 1, ipv.TAR_ADJACENT | ipv.VAN_REVERSE),
+    (synth.BF16, 64, 3, 4, 6, 2, 2, ipv.UNIFORM_SELECT),
 ])
 def test_ckv_loop_matches_oracle(dtype, D, gh, gw, cap_frames, budget_extra, r, mode):
     p = gh * gw
@@ -92,7 +93,8 @@ def test_ckv_loop_with_layer_adaptive_pooling():
 
 @pytest.mark.parametrize("mode,dtype,tau", [(0, synth.BF16, None),
                                             (ipv.TAR_ADJACENT | ipv.HEAD_SHARED, synth.BF16, None),
-                                            (ipv.VAN_REVERSE, synth.F32, (0.3, 0.5, 0.7))])
+                                            (ipv.VAN_REVERSE, synth.F32, (0.3, 0.5, 0.7)),
+                                            (ipv.UNIFORM_SELECT | ipv.HEAD_SHARED, synth.F32, None)])
 def test_ckv_stream_equals_step_by_step(mode, dtype, tau):
     # the library-driven loop against the same loop driven from Python, bit for bit,
     # over three streams that start at different fill levels, in two stretches
@@ -134,6 +136,8 @@ def test_ckv_stream_equals_step_by_step(mode, dtype, tau):
     K2, V2, f2, p2, c2 = fresh()
     n2, pa_ = ipv.ipv_ckv_stream(K2, V2, f2, p2, list(start), fKd[:11], fVd[:11], 0, cap, budget, 0.5, r, tau,
                                  c2.tar, c2.van, c2.keep_idx, c2.ws, gh, gw, mode=mode)
+    # problems only the device sees accumulate in the error word over a call's passes
+    assert c2.device_errors() == 0
     n2, pb_ = ipv.ipv_ckv_stream(K2, V2, f2, p2, n2, fKd[11:], fVd[11:], 11, cap, budget, 0.5, r, tau,
                                  c2.tar, c2.van, c2.keep_idx, c2.ws, gh, gw, mode=mode)
     torch.cuda.synchronize()

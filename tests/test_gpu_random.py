@@ -13,7 +13,8 @@ from tests import parity as P
 pytestmark = pytest.mark.gpu
 
 MODES = [0, ipv.TAR_REVERSE, ipv.VAN_REVERSE, ipv.TAR_ADJACENT, ipv.HEAD_SHARED,
-         ipv.TAR_ADJACENT | ipv.HEAD_SHARED | ipv.VAN_REVERSE]
+         ipv.TAR_ADJACENT | ipv.HEAD_SHARED | ipv.VAN_REVERSE, ipv.UNIFORM_SELECT,
+         ipv.UNIFORM_SELECT | ipv.HEAD_SHARED]
 
 
 def draw(seed):
