@@ -164,22 +164,22 @@ template <typename T, int D>
 __global__ __launch_bounds__(kPrevThreads) void k_prev_van(const T* __restrict__ V, const int32_t* __restrict__ frame_idx,
     const int32_t* __restrict__ patch_idx, int64_t S, int32_t n, int32_t r, int32_t p, int32_t* __restrict__ prev,
     int32_t* __restrict__ first_recent, uint32_t* err, uint32_t* __restrict__ zero, int32_t zero_per_slice,
-    uint32_t prev_padded, uint32_t slices, float* __restrict__ van, int32_t col_blocks, int32_t frame_blocks,
-    uint32_t n_work) {
+    uint32_t prev_padded, uint32_t slices, float* __restrict__ van, TileGrid g) {
   if (blockIdx.x < prev_padded) {
     if (blockIdx.x < slices)
       prev_rows_block(blockIdx.x, frame_idx, patch_idx, S, n, r, p, prev, first_recent, err, zero, zero_per_slice);
     return;
   }
   using C = SweepCfg<T, D>;
-  const uint32_t g = xcd_logical_id(blockIdx.x - prev_padded, gridDim.x - prev_padded);
-  const uint32_t logical = g * 4u + threadIdx.x / 256u;
-  if (logical >= n_work) return;
-  const uint32_t tile = logical / col_blocks;
-  const int64_t slice = tile / frame_blocks;
-  const int32_t f0 = (int32_t)(tile % frame_blocks) * C::U;
-  sweep_tile<T, D, false, true>(V, V, patch_idx, S, n, p, nullptr, n, nullptr, van, err, slice, f0,
-                                (int32_t)(logical % col_blocks), threadIdx.x % 256u);
+  const uint32_t quad = xcd_logical_id(blockIdx.x - prev_padded, g.blocks);
+  const uint32_t logical = quad * 4u + threadIdx.x / 256u;
+  if (logical >= g.n_work) return;
+  const uint32_t tile = fast_div(logical, g.col_blocks);
+  const uint32_t colblock = logical - tile * g.col_blocks.d;
+  const uint32_t slice = fast_div(tile, g.frame_blocks);
+  const uint32_t f0 = (tile - slice * g.frame_blocks.d) * C::U;
+  sweep_tile<T, D, false, true>(V, V, patch_idx, S, n, p, nullptr, n, nullptr, van, err, slice, f0, colblock,
+                                threadIdx.x % 256u);
 }
 
 // TaR of the past rows against their prev rows. Rows are processed in

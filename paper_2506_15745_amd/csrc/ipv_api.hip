@@ -141,6 +141,11 @@ int32_t* ws_pool(void* ws, const Dims& d) {
 
 ipv_status launched() { return hipGetLastError() == hipSuccess ? IPV_OK : IPV_ERR_HIP; }
 
+// blocks: the launch's tile blocks (after any blocks of another role that come first)
+TileGrid tile_grid(int32_t col_blocks, int32_t frame_blocks, uint32_t work, uint32_t blocks) {
+  return TileGrid{make_fastdiv((uint32_t)col_blocks), make_fastdiv((uint32_t)frame_blocks), work, blocks};
+}
+
 uint32_t pad8(uint32_t x) { return (x + 7u) / 8u * 8u; }
 
 // ------------------------------------------------------------ launchers
@@ -171,7 +176,8 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
       const uint32_t prev_padded = pad8((uint32_t)d.slices);
       k_prev_van<T, D><<<dim3(prev_padded + pad8((work + 3) / 4)), dim3(kPrevThreads), 0, st>>>(
           static_cast<const T*>(V), fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws),
-          zero, zero_per_slice, prev_padded, (uint32_t)d.slices, van, col_blocks, frame_blocks, work);
+          zero, zero_per_slice, prev_padded, (uint32_t)d.slices, van,
+          tile_grid(col_blocks, frame_blocks, work, pad8((work + 3) / 4)));
     } else {
       k_prev_rows<<<dim3((uint32_t)d.slices), dim3(kPrevThreads), 0, st>>>(
           fr, pa, d.S, n, r, (int32_t)d.p, ws_prev(ws), ws_first(ws, d), err_word(ws), zero, zero_per_slice);
@@ -197,15 +203,18 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
   const T* k = static_cast<const T*>(K);
   const T* v = static_cast<const T*>(V);
   int32_t* first = ws_first(ws, d);
+  // rows certainly before the recent window (it holds at most r * p rows)
+  const int32_t sure_past = (int32_t)std::max<int64_t>(0, (int64_t)n - (int64_t)r * d.p);
   if (do_tar && do_van) {
     // table and VaN tiles in one launch, then the TaR tiles
     const uint32_t table_padded = pad8(table_real);
     k_table_van<T, D><<<dim3(table_padded + pad8(work)), block, lds, st>>>(
         k, v, fr, pa, d.S, n, r, (int32_t)d.p, blocks, table_padded, table_real, ws_table(ws), first, err_word(ws),
-        zero, zero_per_slice, van, col_blocks, frame_blocks, work);
+        zero, zero_per_slice, van, tile_grid(col_blocks, frame_blocks, work, pad8(work)));
     IPV_TRY(between());
     k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
-                                                             tar, van, err_word(ws), col_blocks, frame_blocks, work);
+                                                             tar, van, err_word(ws),
+                                                             tile_grid(col_blocks, frame_blocks, work, pad8(work)), sure_past);
     return launched();
   }
   if (do_tar)
@@ -215,10 +224,12 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
   IPV_TRY(between());
   if (do_tar)
     k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
-                                                             tar, van, err_word(ws), col_blocks, frame_blocks, work);
+                                                             tar, van, err_word(ws),
+                                                             tile_grid(col_blocks, frame_blocks, work, pad8(work)), sure_past);
   else
     k_score_sweep<T, D, false, true><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
-                                                             tar, van, err_word(ws), col_blocks, frame_blocks, work);
+                                                             tar, van, err_word(ws),
+                                                             tile_grid(col_blocks, frame_blocks, work, pad8(work)), n);
   return launched();
 }
 
@@ -320,7 +331,7 @@ ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa
   }
   k_compact<RB, kCompactThreads, kCompactRows, kCompactColBytes><<<dim3((uint32_t)total), dim3(kCompactThreads), 0, st>>>(
       static_cast<char*>(K), static_cast<char*>(V), fr, pa, d.S, n, budget, keep, err_word(ws), ws_flags(ws, d),
-      chunks);
+      chunks, make_fastdiv((uint32_t)(d.slices * C::PARTS)));
   return launched();
 }
 

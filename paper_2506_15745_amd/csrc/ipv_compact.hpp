@@ -254,17 +254,20 @@ __device__ __forceinline__ void compact_walk(char* __restrict__ K, char* __restr
 }
 
 // grid: slices * PARTS * n_chunks workgroups of NT threads; walk = id % walks,
-// expected chunk = id / walks. flags: walk_words(n_chunks) words per walk.
+// expected chunk = id / walks (walks: a magic-number divisor from the host).
+// flags: walk_words(n_chunks) words per walk.
 template <int RB, int NT, int CHR, int CBMAX>
 __global__ __launch_bounds__(NT) void k_compact(char* __restrict__ K, char* __restrict__ V,
                                                 int32_t* __restrict__ frame_idx, int32_t* __restrict__ patch_idx,
                                                 int64_t S, int32_t n, int32_t budget,
                                                 const int32_t* __restrict__ keep_idx, uint32_t* err,
-                                                uint32_t* flags, uint32_t n_chunks) {
+                                                uint32_t* flags, uint32_t n_chunks, FastDiv walks) {
   using C = CompactCfg<RB, NT, CHR, CBMAX>;
   __shared__ CompactShared<NT, CHR> sh;
-  const uint32_t walks = gridDim.x / n_chunks;
-  const uint32_t kexp = blockIdx.x / walks, w = blockIdx.x % walks;
+  // every argument in the first round of scalar loads
+  asm volatile("" ::"s"(K), "s"(V), "s"(frame_idx), "s"(patch_idx), "s"(S), "s"(n), "s"(budget), "s"(keep_idx),
+               "s"(err), "s"(flags), "s"(n_chunks), "s"(walks.d), "s"(walks.m), "s"(walks.s2));
+  const uint32_t kexp = fast_div(blockIdx.x, walks), w = blockIdx.x - kexp * walks.d;
   compact_walk<RB, NT, CHR, CBMAX>(K, V, frame_idx, patch_idx, S, n, budget, keep_idx, err,
                                    flags + (int64_t)w * walk_words(n_chunks), n_chunks, w / C::PARTS,
                                    (int)(w % C::PARTS), kexp, sh);

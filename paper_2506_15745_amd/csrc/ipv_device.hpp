@@ -94,6 +94,7 @@ constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int kDppRowShr = 0x110;     // + k: row_shr:k (within rows of 16 lanes)
 constexpr int kDppRowMirror = 0x140;  // lane l <- 15 - l within a row
 constexpr int kDppHalfMirror = 0x141; // lane l <- 7 - l within each 8 lanes
+constexpr int kDppQuadMirror = 0x1B;  // quad_perm [3,2,1,0]: lane l <- 3 - l within each 4 lanes
 
 template <int CTRL, bool BOUND_ZERO = false>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
@@ -120,6 +121,61 @@ __device__ __forceinline__ float group_sum(float v) {
   if (G >= 32) v += __shfl_xor(v, 16, kWave);
   if (G >= 64) v += __shfl_xor(v, 32, kWave);
   return v;
+}
+
+// Reduce-scatter of four rows' partial sums over an aligned group of G lanes
+// (G a power of two, 4 <= G <= 64): v[u][m] is this lane's part of value m of
+// row u. On return the lane holds out[m] = the group's total of value m for
+// row scatter_row<G>(lane), the same in all G / 4 lanes that hold that row.
+// Two exchange steps halve the rows a lane keeps (it adds the partner's part
+// of the rows it keeps and hands over the others): partners are the lane
+// mirrored across the group's halves, then across its quarters; the quarter
+// of lanes that ends up with one row then sums over its own lanes. Groups
+// wider than 16 lanes first fold onto 16 through the crossbar.
+template <int G>
+__device__ __forceinline__ int scatter_row(int lane) {
+  constexpr int H = G > 16 ? 16 : G;
+  return ((lane & (H / 2)) ? 2 : 0) + ((lane & (H / 4)) ? 1 : 0);
+}
+
+template <int G, int M>
+__device__ __forceinline__ void reduce_scatter4(float (&v)[4][M], float (&out)[M], int lane) {
+  static_assert(G >= 4 && G <= 64 && (G & (G - 1)) == 0, "group of 4..64 lanes");
+  if (G >= 32) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        v[u][m] += __shfl_xor(v[u][m], 16, kWave);
+        if (G == 64) v[u][m] += __shfl_xor(v[u][m], 32, kWave);
+      }
+  }
+  constexpr int H = G > 16 ? 16 : G;
+  // mirror across halves, then across quarters, of an H-lane group
+  constexpr int MA = H == 16 ? kDppRowMirror : (H == 8 ? kDppHalfMirror : kDppXor2);
+  constexpr int MB = H == 16 ? kDppHalfMirror : (H == 8 ? kDppQuadMirror : kDppXor1);
+  const bool hi_a = (lane & (H / 2)) != 0, hi_b = (lane & (H / 4)) != 0;
+  float w[2][M];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      const float keep = hi_a ? v[2 + j][m] : v[j][m];
+      const float give = hi_a ? v[j][m] : v[2 + j][m];
+      w[j][m] = keep + dpp_f32<MA>(give);
+    }
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    const float keep = hi_b ? w[1][m] : w[0][m];
+    const float give = hi_b ? w[0][m] : w[1][m];
+    out[m] = keep + dpp_f32<MB>(give);
+    if (H == 16) {
+      out[m] += dpp_f32<kDppXor1>(out[m]);
+      out[m] += dpp_f32<kDppXor2>(out[m]);
+    } else if (H == 8) {
+      out[m] += dpp_f32<kDppXor1>(out[m]);
+    }
+  }
 }
 
 // Inclusive prefix sum over the 64 lanes of a fully active wave: a
@@ -186,6 +242,33 @@ __device__ inline uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
   if (u == 0x80000000u) u = 0u;
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Division by a divisor d fixed for a launch, as a multiply-high and two
+// shifts with a magic number computed on the host (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", 1994): exact for
+// every 32-bit x. With l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1:
+//   t = mulhi(x, m),  x / d = (t + ((x - t) >> 1)) >> (l - 1);
+// d = 1 uses m = 0 and no shifts.
+struct FastDiv {
+  uint32_t d, m, s1, s2;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f{d, 0u, 0u, 0u};
+  if (d > 1) {
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    f.m = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+    f.s1 = 1;
+    f.s2 = l - 1;
+  }
+  return f;
+}
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t x, const FastDiv& f) {
+  const uint32_t t = __umulhi(x, f.m);
+  return (t + ((x - t) >> f.s1)) >> f.s2;
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (id % 8). Renumber

@@ -206,21 +206,33 @@ struct SweepCfg {
   static constexpr int U = 4;
 };
 
+// Where a launch's tiles are: work item w (after the XCD renumbering) is
+// column block w % col_blocks of frame block (w / col_blocks) % frame_blocks
+// of slice w / (col_blocks * frame_blocks); the divisions are magic-number
+// multiplies, so a tile finds its place in a few scalar instructions.
+struct TileGrid {
+  FastDiv col_blocks, frame_blocks;
+  uint32_t n_work;
+  uint32_t blocks;  // tile blocks of the launch (a multiple of 8), the XCD renumbering's grid
+};
+
 // One tile: 256 threads (tid in [0, 256)), columns [colblock * GROUPS, +GROUPS),
-// frames [f0, f0 + U). rec = the slice's first recent row.
+// frames [f0, f0 + U). rec = the slice's first recent row. Row indices are
+// 32-bit (a slice holds at most 65536 rows).
 template <typename T, int D, bool TAR, bool VAN>
-__device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __restrict__ V, const int32_t* __restrict__ patch_idx,
-                           int64_t S, int32_t n, int32_t p, const float* __restrict__ table, int32_t rec,
-                           float* __restrict__ tar, float* __restrict__ van, uint32_t* err, int64_t slice,
-                           int32_t f0, int32_t colblock, int tid) {
+__device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __restrict__ V,
+                                           const int32_t* __restrict__ patch_idx, int64_t S, uint32_t n, uint32_t p,
+                                           const float* __restrict__ table, uint32_t rec, float* __restrict__ tar,
+                                           float* __restrict__ van, uint32_t* err, uint32_t slice, uint32_t f0,
+                                           uint32_t colblock, int tid) {
   using C = SweepCfg<T, D>;
   constexpr int EPL = C::EPL, LPR = C::LPR, GROUPS = C::GROUPS, U = C::U;
-  const int32_t col = colblock * GROUPS + tid / LPR;
+  const uint32_t col = colblock * GROUPS + tid / LPR;
   const int lane = tid % LPR;
   if (col >= p) return;  // the whole lane group idles: it is in no cross-lane sum
-  const int64_t base = slice * S;
+  const int64_t base = (int64_t)slice * S;
   if (!TAR) rec = n;
-  const float* mtab = table + (int64_t)slice * p * D + lane * EPL;
+  const uint32_t past_end = min(n, rec);  // rows [0, past_end) are past (TaR); VaN scores rows [0, n)
 
   // Every load is a buffer load issued without a branch (a lane with nothing
   // to read uses an offset past the end and gets zeros); the patch ids of
@@ -233,40 +245,40 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
   int32_t pq_mine = 0;
   if (TAR) {
     const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(patch_idx + base, (uint32_t)(S * 4));
-    const int64_t xm = (int64_t)(f0 + (lane & 3)) * p + col;
-    pq_mine = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, (xm < n && xm < rec) ? (uint32_t)xm * 4u : kSkip,
-                                                            0, 0);
+    const uint32_t xm = (f0 + (lane & 3)) * p + col;
+    pq_mine = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, xm < past_end ? xm * 4u : kSkip, 0, 0);
   }
   Raw16 kr[U], vr[U];
   const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(K + base * D, (uint32_t)S * RB);
   const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(V + base * D, (uint32_t)S * RB);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const int64_t x = (int64_t)(f0 + u) * p + col;
+    const uint32_t x = (f0 + u) * p + col;
     if (TAR) {
-      const auto k = __builtin_amdgcn_raw_buffer_load_b128(krs, (x < n && x < rec) ? (uint32_t)x * RB + lo : kSkip, 0, 0);
+      const auto k = __builtin_amdgcn_raw_buffer_load_b128(krs, x < past_end ? x * RB + lo : kSkip, 0, 0);
       kr[u].w[0] = k[0];
       kr[u].w[1] = k[1];
       kr[u].w[2] = k[2];
       kr[u].w[3] = k[3];
     }
     if (VAN) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(vrs, x < n ? (uint32_t)x * RB + lo : kSkip, 0, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(vrs, x < n ? x * RB + lo : kSkip, 0, 0);
       vr[u].w[0] = v[0];
       vr[u].w[1] = v[1];
       vr[u].w[2] = v[2];
       vr[u].w[3] = v[3];
     }
   }
+  // the m vector of the column's own position, fetched with the K loads
   float4 ms[EPL / 4];
-  const bool any_past = TAR && (int64_t)f0 * p + col < min(n, rec);
+  const bool any_past = TAR && f0 * p + col < past_end;
   if (TAR) {
     // the resource base must be uniform: the slice's table, lane offset in the offset
-    const __amdgpu_buffer_rsrc_t mrs = buffer_rsrc(table + (int64_t)slice * p * D, (uint32_t)(p * D * 4));
+    const __amdgpu_buffer_rsrc_t mrs = buffer_rsrc(table + (int64_t)slice * p * D, p * D * 4u);
 #pragma unroll
     for (int i = 0; i < EPL / 4; ++i) {
       const auto m = __builtin_amdgcn_raw_buffer_load_b128(
-          mrs, any_past ? (uint32_t)(col * D + lane * EPL + 4 * i) * 4u : kSkip, 0, 0);
+          mrs, any_past ? (col * D + lane * EPL + 4 * i) * 4u : kSkip, 0, 0);
       ms[i] = make_float4(__uint_as_float(m[0]), __uint_as_float(m[1]), __uint_as_float(m[2]),
                           __uint_as_float(m[3]));
     }
@@ -278,32 +290,37 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
     pq[2] = (int32_t)dpp_u32<0xAA>((uint32_t)pq_mine);
     pq[3] = (int32_t)dpp_u32<0xFF>((uint32_t)pq_mine);
   }
-  // Scores: every lane of a group ends up with all U sums; lane u of the
-  // group stores row u, so a wave stores each score column with one
-  // instruction instead of U.
-  float vsc[U], tsc[U];
+  // Each lane's partial sums of the U rows are reduce-scattered over the lane
+  // group, so that a lane ends up with the totals of one row (scatter_row)
+  // and the lanes that hold row u store it: one store instruction per wave.
+  constexpr int Q = (LPR > 16 ? 16 : LPR) / 4;  // lanes per row after the scatter
+  const int my_row = scatter_row<LPR>(lane);
+  const uint32_t x_mine = (f0 + my_row) * p + col;
+  const bool storer = lane < 16 && lane % Q == 0 && x_mine < n;
   if (VAN) {
+    float part[U][1];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t x = (int64_t)(f0 + u) * p + col;
-      const float ss = x < n ? Lane<T>::sumsq(vr[u]) : 0.f;
-      vsc[u] = fast_sqrt(group_sum<LPR>(ss));
-    }
+    for (int u = 0; u < U; ++u) part[u][0] = (f0 + u) * p + col < n ? Lane<T>::sumsq(vr[u]) : 0.f;
+    float tot[1];
+    reduce_scatter4<LPR, 1>(part, tot, lane);
+    if (storer) van[base + x_mine] = fast_sqrt(tot[0]);
   }
   if (TAR) {
+    float part[U][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t x = (int64_t)(f0 + u) * p + col;
-      const bool past = x < n && x < rec;
+      const uint32_t x = (f0 + u) * p + col;
+      const bool past = x < past_end;
       const int32_t q = pq[u];
-      const bool ok = past && q >= 0 && q < p;
+      const bool ok = past && q >= 0 && q < (int32_t)p;
       if (past && !ok && lane == 0) raise_error(err, 1u);
       float4 m[EPL / 4];
 #pragma unroll
       for (int i = 0; i < EPL / 4; ++i) m[i] = ms[i];
-      if (ok && q != col) {  // the row is not at its frame-plane position: exact lookup
+      if (ok && q != (int32_t)col) {  // the row is not at its frame-plane position: exact lookup
+        const float* mq = table + ((int64_t)slice * p + q) * D + lane * EPL;
 #pragma unroll
-        for (int i = 0; i < EPL / 4; ++i) m[i] = *reinterpret_cast<const float4*>(mtab + (int64_t)q * D + 4 * i);
+        for (int i = 0; i < EPL / 4; ++i) m[i] = *reinterpret_cast<const float4*>(mq + 4 * i);
       }
       float dot = 0.f, kk = 0.f;
       if (ok) {
@@ -316,40 +333,45 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
         }
         kk = Lane<T>::sumsq(kr[u]);
       }
-      dot = group_sum<LPR>(dot);
-      kk = group_sum<LPR>(kk);
-      float sc = kk != 0.f ? -(dot * fast_rsqrt(kk)) : 0.f;  // a NaN key gives NaN, as in exact arithmetic
-      if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
-      tsc[u] = past ? sc : 0.f;
+      part[u][0] = dot;
+      part[u][1] = kk;
     }
-  }
-  if (lane < U) {
-    const int64_t x = (int64_t)(f0 + lane) * p + col;
-    if (x < n) {
-      if (VAN) van[base + x] = lane == 0 ? vsc[0] : lane == 1 ? vsc[1] : lane == 2 ? vsc[2] : vsc[3];
-      if (TAR) tar[base + x] = lane == 0 ? tsc[0] : lane == 1 ? tsc[1] : lane == 2 ? tsc[2] : tsc[3];
-    }
+    float tot[2];
+    reduce_scatter4<LPR, 2>(part, tot, lane);
+    float sc = tot[1] != 0.f ? -(tot[0] * fast_rsqrt(tot[1])) : 0.f;  // a NaN key gives NaN, as in exact arithmetic
+    if (sc == 0.f) sc = 0.f;  // -0.0 -> +0.0
+    if (storer) tar[base + x_mine] = x_mine < past_end ? sc : 0.f;
   }
 }
 
-// grid: padded to a multiple of 8; work w = (slice * frame_blocks + frame block) * col_blocks + column block
+// The kernel arguments a tile needs, all read in the first round of scalar
+// loads (an empty asm statement that takes them as operands keeps the
+// compiler from spreading the loads over several dependent rounds).
+#define IPV_ARGS_NOW(...) asm volatile("" ::__VA_ARGS__)
+
+// grid: padded to a multiple of 8; work w = (slice * frame_blocks + frame block) * col_blocks + column block.
+// sure_past: rows below it are past whatever the frame ids say (n - r * p:
+// the window holds at most r frames of at most p rows), so a tile that ends
+// there does not wait for the slice's window start.
 template <typename T, int D, bool TAR, bool VAN>
 __global__ __launch_bounds__(256) void k_score_sweep(const T* __restrict__ K, const T* __restrict__ V,
                                                      const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
                                                      int32_t p, const float* __restrict__ table,
                                                      const int32_t* __restrict__ first_recent,
                                                      float* __restrict__ tar, float* __restrict__ van,
-                                                     uint32_t* err, int32_t col_blocks, int32_t frame_blocks,
-                                                     uint32_t n_work) {
+                                                     uint32_t* err, TileGrid g, int32_t sure_past) {
   using C = SweepCfg<T, D>;
-  const uint32_t logical = xcd_logical_id(blockIdx.x, gridDim.x);
-  if (logical >= n_work) return;
-  const uint32_t tile = logical / col_blocks;
-  const int64_t slice = tile / frame_blocks;
-  const int32_t f0 = (int32_t)(tile % frame_blocks) * C::U;
-  const int32_t rec = TAR ? first_recent[slice] : n;
-  sweep_tile<T, D, TAR, VAN>(K, V, patch_idx, S, n, p, table, rec, tar, van, err, slice, f0,
-                             (int32_t)(logical % col_blocks), threadIdx.x);
+  IPV_ARGS_NOW("s"(K), "s"(V), "s"(patch_idx), "s"(S), "s"(n), "s"(p), "s"(table), "s"(first_recent), "s"(tar),
+               "s"(van), "s"(g.col_blocks.m), "s"(g.frame_blocks.m), "s"(g.n_work), "s"(g.blocks), "s"(sure_past));
+  const uint32_t logical = xcd_logical_id(blockIdx.x, g.blocks);
+  if (logical >= g.n_work) return;
+  const uint32_t tile = fast_div(logical, g.col_blocks);
+  const uint32_t colblock = logical - tile * g.col_blocks.d;
+  const uint32_t slice = fast_div(tile, g.frame_blocks);
+  const uint32_t f0 = (tile - slice * g.frame_blocks.d) * C::U;
+  const bool tail = (int64_t)(f0 + C::U) * p > sure_past;
+  const uint32_t rec = TAR && tail ? (uint32_t)first_recent[slice] : (uint32_t)n;
+  sweep_tile<T, D, TAR, VAN>(K, V, patch_idx, S, n, p, table, rec, tar, van, err, slice, f0, colblock, threadIdx.x);
 }
 
 // The recent-key table and the VaN half of the sweep in one launch. The VaN
@@ -368,8 +390,7 @@ __global__ __launch_bounds__(256) void k_table_van(const T* __restrict__ K, cons
                                                    uint32_t table_padded, uint32_t table_real,
                                                    float* __restrict__ table, int32_t* __restrict__ first_recent,
                                                    uint32_t* err, uint32_t* __restrict__ zero, int32_t zero_per_slice,
-                                                   float* __restrict__ van, int32_t col_blocks, int32_t frame_blocks,
-                                                   uint32_t n_work) {
+                                                   float* __restrict__ van, TileGrid g) {
   extern __shared__ int32_t slot[];
   if (blockIdx.x < table_padded) {
     if (blockIdx.x < table_real)
@@ -378,13 +399,16 @@ __global__ __launch_bounds__(256) void k_table_van(const T* __restrict__ K, cons
     return;
   }
   using C = SweepCfg<T, D>;
-  const uint32_t logical = xcd_logical_id(blockIdx.x - table_padded, gridDim.x - table_padded);
-  if (logical >= n_work) return;
-  const uint32_t tile = logical / col_blocks;
-  const int64_t slice = tile / frame_blocks;
-  const int32_t f0 = (int32_t)(tile % frame_blocks) * C::U;
-  sweep_tile<T, D, false, true>(K, V, patch_idx, S, n, p, table, n, nullptr, van, err, slice, f0,
-                                (int32_t)(logical % col_blocks), threadIdx.x);
+  IPV_ARGS_NOW("s"(V), "s"(S), "s"(n), "s"(p), "s"(van), "s"(g.col_blocks.m), "s"(g.frame_blocks.m),
+               "s"(g.n_work), "s"(g.blocks));
+  const uint32_t logical = xcd_logical_id(blockIdx.x - table_padded, g.blocks);
+  if (logical >= g.n_work) return;
+  const uint32_t tile = fast_div(logical, g.col_blocks);
+  const uint32_t colblock = logical - tile * g.col_blocks.d;
+  const uint32_t slice = fast_div(tile, g.frame_blocks);
+  const uint32_t f0 = (tile - slice * g.frame_blocks.d) * C::U;
+  sweep_tile<T, D, false, true>(K, V, patch_idx, S, n, p, table, n, nullptr, van, err, slice, f0, colblock,
+                                threadIdx.x);
 }
 
 // ---------------------------------------------------------------- adaptive pooling
