@@ -89,5 +89,10 @@ POOL = Workload(
     value_sigma=(0.1, 0.35, 0.55, 1.0), cv_tau=(0.3, 0.5, 0.7),
     note="7B-class shape with per-layer value spread cycling so every pooling size 7/5/3/1 occurs")
 
+ONE_LAYER = Workload(
+    name="7b-class-1L", streams=1, layers=1, kv_heads=4, head_dim=128, grid_h=14, grid_w=14,
+    n_tokens=6272, budget=3136, recent_frames=4, alphas=(0.5,), dtype=BF16, seeds=(1,), rho_specs=(_U099,),
+    note="one layer of the 7B-class cache (4 KV heads, 6272 -> 3136 rows): the latency of a single-layer pass")
+
 ALL = (TINY, SEVEN_B, STREAMING, SEVENTY_B, BATCHED)
-BY_NAME = {w.name: w for w in ALL + (POOL,)}
+BY_NAME = {w.name: w for w in ALL + (POOL, ONE_LAYER)}
