@@ -127,6 +127,7 @@ def test_slice_bytes_beyond_32_bit_offsets_rejected():
 def test_rows_above_select_limit_rejected():
     s = shape(capacity=70000)
     assert call_compress(s, n=70000, budget=35000, wsb=1 << 40) == ipv.ERR_SHAPE
+    assert call_compress(s, n=65537, budget=35000, wsb=1 << 40) == ipv.ERR_SHAPE  # one above the limit
 
 
 def test_entry_points_validate_their_own_arguments():

@@ -128,6 +128,24 @@ def test_degenerate_budgets():
             assert np.array_equal(got.keep[0, 0, 0], np.arange(n - R, n))
 
 
+@pytest.mark.parametrize("dtype,D,gh,gw,n,S,r,budget,alpha", [
+    # the largest count a slice takes (1024 selection threads x 64 rows), 16-byte row runs
+    (synth.BF16, 64, 16, 16, 65536, 65536, 4, 32768, 0.5),
+    # one row fewer, a capacity that is not a multiple of 4 (4-byte row loads), a
+    # ragged last frame and a 256-frame recent window
+    (synth.F32, 32, 7, 9, 65535, 65535, 256, 40000, 0.3),
+    # the longest recent window with the narrowest bf16 rows: the table's slot
+    # array at its largest (64 position groups x 256 frames of LDS)
+    (synth.BF16, 32, 2, 2, 4099, 4100, 256, 2048, 0.5),
+])
+def test_largest_sizes(dtype, D, gh, gw, n, S, r, budget, alpha):
+    w = W.Workload(name="largest-D%d-r%d" % (D, r), streams=1, layers=1, kv_heads=2, head_dim=D, grid_h=gh, grid_w=gw,
+                   n_tokens=n, budget=budget, recent_frames=r, alphas=(alpha,), dtype=dtype, seeds=(31,),
+                   rho_specs=(synth.RhoSpec(0.0, 0.99, static_frac=0.2, static_rho=0.999),))
+    K, V, fr, pa = cache_of(w, capacity=S)
+    full_check(w, K, V, fr, pa, alpha)
+
+
 def test_pool_workload():
     w = W.POOL
     got = full_check(w, *cache_of(w), 0.5, steps=True, tau=w.cv_tau)
