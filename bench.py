@@ -418,6 +418,7 @@ def main():
         record(bounds[j], cur)
         step(i)
     record(bounds[args.steps], cur)
+    enqueue = time.perf_counter() - t0  # host time to enqueue the timed passes
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     pass_us = [hip.elapsed_ms(bounds[j], bounds[j + 1]) * 1e3 for j in range(args.steps)]
@@ -496,7 +497,8 @@ def main():
                        "p50": round(pct(pass_us, 0.5), 2), "p99": round(pct(pass_us, 0.99), 2),
                        "source": "events at the timed loop's pass boundaries",
                        "warm_mean": round(statistics.mean(warm_us), 2), "warm_p50": round(pct(warm_us, 0.5), 2),
-                       "warm_source": "events around passes on caches restored right before them, no eviction"},
+                       "warm_source": "events around passes on caches restored right before them, no eviction",
+                       "host_enqueue_per_pass": round(enqueue / args.steps * 1e6, 2)},
         "pct_of_peak_hbm": round(100 * value / PEAK_HBM_GBPS, 2),
         "tokens_per_s": round(B * w.n_tokens / (ms_per_step * 1e-3), 1),
         "rows_per_s": round(B * L * H * w.n_tokens / (ms_per_step * 1e-3), 1),
