@@ -263,7 +263,14 @@ __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t v) {
   if (i < count) p[i] = v;
 }
 
-constexpr int kSelThreads = 1024;
+constexpr int kSelThreads = 1024;  // most threads of a selection workgroup
+
+// Threads of a selection workgroup: whole waves for the n rows at RPT rows a
+// thread, at most kSelThreads (the caller picks RPT >= n / kSelThreads).
+uint32_t sel_threads(int32_t n, int RPT) {
+  const int32_t t = (n + RPT - 1) / RPT;
+  return (uint32_t)std::min(kSelThreads, (t + 63) / 64 * 64);
+}
 
 // mode: the reverse bits complement a stage's keys; IPV_HEAD_SHARED gives one
 // block (and one keep set) to each (stream, layer)
@@ -273,14 +280,14 @@ ipv_status run_select(const Dims& d, const float* tar, const float* van, const i
   const int32_t heads = (mode & IPV_HEAD_SHARED) ? (int32_t)d.H : 1;
   const uint32_t tflip = (mode & IPV_TAR_REVERSE) ? 0xffffffffu : 0u;
   const uint32_t vflip = (mode & IPV_VAN_REVERSE) ? 0xffffffffu : 0u;
-  const dim3 grid((uint32_t)(d.slices / heads));
+  const dim3 grid((uint32_t)(d.slices / heads)), block(sel_threads(n, RPT));
   // 16-byte row-run loads need every slice to start 16-byte aligned
   if (d.S % 4 == 0)
-    k_select<kSelThreads, RPT, true><<<grid, dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget, tar_total, r,
-                                                                         keep, err, heads, tflip, vflip);
+    k_select<kSelThreads, RPT, true><<<grid, block, 0, st>>>(tar, van, fr, d.S, n, budget, tar_total, r, keep, err,
+                                                             heads, tflip, vflip);
   else
-    k_select<kSelThreads, RPT, false><<<grid, dim3(kSelThreads), 0, st>>>(tar, van, fr, d.S, n, budget, tar_total,
-                                                                          r, keep, err, heads, tflip, vflip);
+    k_select<kSelThreads, RPT, false><<<grid, block, 0, st>>>(tar, van, fr, d.S, n, budget, tar_total, r, keep, err,
+                                                              heads, tflip, vflip);
   return launched();
 }
 
@@ -289,13 +296,11 @@ template <int RPT>
 ipv_status run_uniform(const Dims& d, const int32_t* fr, int32_t n, int32_t budget, int32_t r, int32_t* keep,
                        uint32_t* err, hipStream_t st, uint32_t mode) {
   const int32_t heads = (mode & IPV_HEAD_SHARED) ? (int32_t)d.H : 1;
-  const dim3 grid((uint32_t)(d.slices / heads));
+  const dim3 grid((uint32_t)(d.slices / heads)), block(sel_threads(n, RPT));
   if (d.S % 4 == 0)
-    k_select_uniform<kSelThreads, RPT, true><<<grid, dim3(kSelThreads), 0, st>>>(fr, d.S, n, budget, r, keep, err,
-                                                                                 heads);
+    k_select_uniform<kSelThreads, RPT, true><<<grid, block, 0, st>>>(fr, d.S, n, budget, r, keep, err, heads);
   else
-    k_select_uniform<kSelThreads, RPT, false><<<grid, dim3(kSelThreads), 0, st>>>(fr, d.S, n, budget, r, keep, err,
-                                                                                  heads);
+    k_select_uniform<kSelThreads, RPT, false><<<grid, block, 0, st>>>(fr, d.S, n, budget, r, keep, err, heads);
   return launched();
 }
 

@@ -1,6 +1,8 @@
-// Keep-set selection (Algorithm 1 steps (3)-(5); Sec. 3.3), one workgroup of
-// NT threads per (stream, layer, head) slice, or per (stream, layer) when the
-// heads share one keep set.
+// Keep-set selection (Algorithm 1 steps (3)-(5); Sec. 3.3), one workgroup per
+// (stream, layer, head) slice, or per (stream, layer) when the heads share one
+// keep set. A workgroup has as many waves as its rows need, at most NT / 64
+// (the host fits the launch); per-wave LDS slots of absent waves hold neutral
+// values, so loops over all NT / 64 slots see only the present ones.
 //
 // Variants: a reversed stage (the TaR Reverse / VaN Reverse rows of Tab. 5)
 // complements its keys, so the same top-k takes the lowest scores, ties still
@@ -26,14 +28,19 @@
 //     barrier that also publishes the window start (the VaN range is taken
 //     over all past rows, a superset of its candidates, which still bounds
 //     their common prefix);
-//   * a digit costs one barrier: after it, every wave reads the whole
-//     histogram and finds the threshold digit itself (the same answer in all
-//     waves). Histograms rotate over three LDS buffers, so a buffer is
-//     cleared only after the barrier that follows its last reader;
+//   * a digit costs two barriers: after the histogram's, wave 0 alone reads
+//     it and finds the threshold digit, and publishes it for the second.
+//     (Every wave repeating the scan saves that barrier but costs more: four
+//     waves share a SIMD, so sixteen copies of the scan queue for issue.)
+//     Histograms rotate over three LDS buffers, so a buffer is cleared only
+//     after the barrier that follows its last reader;
 //   * each histogram has kHistCopies copies, lane l adding into copy
 //     l % kHistCopies, so lanes of one wave that hit the same bin mostly hit
 //     different words in different banks;
-//   * scans take one barrier: each wave adds up the wave totals it needs.
+//   * scans take one barrier: each wave adds up the wave totals it needs;
+//   * the keep set is gathered in LDS in output order, then written with
+//     consecutive stores (up to kStageRows rows; larger budgets store from
+//     the threads that own the rows).
 #pragma once
 
 #include "ipv_device.hpp"
@@ -47,6 +54,7 @@ constexpr int kHistCopies = 4;
 constexpr int kHistSkew = 4;
 constexpr int kHistStride = 256 + kHistSkew;
 constexpr int kHistWords = kHistCopies * kHistStride;
+constexpr int kStageRows = 8192;  // keep sets up to this size are gathered in LDS before the stores
 
 template <int NT>
 struct SelShared {
@@ -57,7 +65,21 @@ struct SelShared {
   uint32_t wave_bad[NW];
   int32_t wave_tot[3][NW];                    // [TaR ties, VaN ties, output positions]
   int32_t first_recent;
+  int32_t dig[3];                             // a digit's threshold digit, keys above it, keys in it
+  int32_t stage[kStageRows];                  // the keep set in output order
 };
+
+// Neutral per-wave slots for the waves the launch does not have.
+template <int NT>
+__device__ __forceinline__ void neutral_missing_waves(SelShared<NT>& sh) {
+  const int t = threadIdx.x, nw = (int)(blockDim.x / kWave);
+  if (t >= nw && t < NT / kWave) {
+    sh.wave_min[0][t] = sh.wave_min[1][t] = sh.late_min[t] = 0xffffffffu;
+    sh.wave_max[0][t] = sh.wave_max[1][t] = sh.late_max[t] = 0u;
+    sh.wave_bad[t] = 0u;
+    sh.wave_tot[0][t] = sh.wave_tot[1][t] = sh.wave_tot[2][t] = 0;
+  }
+}
 
 // State of one stage's digit loop, the same in every thread.
 struct Radix {
@@ -90,31 +112,35 @@ __device__ __forceinline__ Radix radix_digits(const uint32_t (&key)[RPT], uint64
         atomicAdd(&h[copy * kHistStride + ((key[i] >> shift) & dmask)], 1u);
     // the next digit's buffer, last read two digits ago
     uint32_t* nxt = sh.hist[buf == 2 ? 0 : buf + 1];
-    for (int i = tid; i < kHistWords; i += NT) nxt[i] = 0u;
+    for (int i = tid; i < kHistWords; i += (int)blockDim.x) nxt[i] = 0u;
     __syncthreads();
-    // every wave: lane l holds digits 255-4l .. 252-4l (descending digit order),
-    // read as one 16-byte run of bins 252-4l .. 255-4l per copy
-    int32_t c[4] = {0, 0, 0, 0};
+    if (tid < kWave) {
+      // wave 0: lane l holds digits 255-4l .. 252-4l (descending digit order),
+      // read as one 16-byte run of bins 252-4l .. 255-4l per copy
+      int32_t c[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int cp = 0; cp < kHistCopies; ++cp) {
-      const uint4 v = *reinterpret_cast<const uint4*>(h + cp * kHistStride + 252 - 4 * lane);
-      c[0] += (int32_t)v.w;
-      c[1] += (int32_t)v.z;
-      c[2] += (int32_t)v.y;
-      c[3] += (int32_t)v.x;
+      for (int cp = 0; cp < kHistCopies; ++cp) {
+        const uint4 v = *reinterpret_cast<const uint4*>(h + cp * kHistStride + 252 - 4 * lane);
+        c[0] += (int32_t)v.w;
+        c[1] += (int32_t)v.z;
+        c[2] += (int32_t)v.y;
+        c[3] += (int32_t)v.x;
+      }
+      const int32_t s = c[0] + c[1] + c[2] + c[3];
+      const int32_t incl = wave_inclusive_scan(s);
+      const int32_t excl = incl - s;
+      // the lane holding the threshold digit: the one whose run of bins
+      // reaches the remaining count (exactly one lane)
+      if (excl < R.remaining && R.remaining <= incl) {
+        int32_t above = excl, j = 0;
+        while (j < 3 && above + c[j] < R.remaining) above += c[j++];
+        sh.dig[0] = 255 - 4 * lane - j;
+        sh.dig[1] = above;
+        sh.dig[2] = j == 0 ? c[0] : (j == 1 ? c[1] : (j == 2 ? c[2] : c[3]));
+      }
     }
-    const int32_t s = c[0] + c[1] + c[2] + c[3];
-    const int32_t incl = wave_inclusive_scan(s);
-    const int32_t excl = incl - s;
-    const uint64_t hit = __ballot(excl < R.remaining && R.remaining <= incl);
-    const int L = __ffsll((unsigned long long)hit) - 1;  // the lane holding the threshold digit
-    int32_t above = excl, j = 0;
-    while (j < 3 && above + c[j] < R.remaining) above += c[j++];
-    const int32_t digit = 255 - 4 * lane - j;
-    const int32_t bin = j == 0 ? c[0] : (j == 1 ? c[1] : (j == 2 ? c[2] : c[3]));
-    const int32_t d = __builtin_amdgcn_readlane(digit, L);
-    const int32_t a = __builtin_amdgcn_readlane(above, L);
-    const int32_t cnt = __builtin_amdgcn_readlane(bin, L);
+    __syncthreads();
+    const int32_t d = sh.dig[0], a = sh.dig[1], cnt = sh.dig[2];
     R.remaining -= a;
     R.prefix |= (uint32_t)d << shift;
     R.pmask |= dmask << shift;
@@ -233,6 +259,26 @@ __device__ __forceinline__ bool heads_differ(const int32_t* __restrict__ fr0, in
   return diff;
 }
 
+// Writes the keep set: `kept` marks this thread's kept rows among its RPT
+// rows from row0, `pos` is the number of kept rows before them. `put(j, row)`
+// stores output position j. Sets of up to kStageRows rows are gathered in LDS
+// first, so that the global stores are consecutive across the block.
+template <int NT, int RPT, typename Put>
+__device__ __forceinline__ void write_keep(uint64_t kept, int32_t pos, int32_t budget, int64_t row0,
+                                           SelShared<NT>& sh, Put put) {
+  if (budget > kStageRows) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i)
+      if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i)
+    if (((kept >> i) & 1ull) && pos < budget) sh.stage[pos++] = (int32_t)(row0 + i);
+  __syncthreads();
+  for (int32_t j = threadIdx.x; j < budget; j += (int32_t)blockDim.x) put(j, sh.stage[j]);
+}
+
 // One group of `heads` slices (1: a slice of its own) with NT threads. VEC:
 // every slice's row 0 is 16-byte aligned (capacity % 4 == 0) so row runs
 // load 16 bytes at a time. tflip / vflip: 0, or ~0 for a reversed stage.
@@ -268,7 +314,8 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   const int32_t prev_row = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, (uint32_t)max(row0 - 1, (int64_t)0) * 4u,
                                                                           0, 0);
   const int32_t before = row0 > 0 ? prev_row : INT32_MIN;
-  for (int i = tid; i < kHistWords; i += NT) sh.hist[0][i] = 0u;
+  for (int i = tid; i < kHistWords; i += (int)blockDim.x) sh.hist[0][i] = 0u;
+  neutral_missing_waves<NT>(sh);
 
   const int64_t thr = (int64_t)last - r + 1;
   uint64_t valid = 0, recent = 0;
@@ -333,7 +380,7 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   if (broken) {
     // metadata breaks the cache invariants: report, and keep rows 0..C-1 in place
     if (tid == 0) raise_error(err, any_bad ? 2u : 4u);
-    for (int32_t j = tid; j < budget; j += NT) put(j, j);
+    for (int32_t j = tid; j < budget; j += (int32_t)blockDim.x) put(j, j);
     return;
   }
   const int32_t b_tar = max(0, tar_total - n_recent);
@@ -364,9 +411,7 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   int32_t total;
   int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh.wave_tot[2], &total);
   if (total != budget && tid == 0) raise_error(err, 16u);  // only reachable with NaN keys
-#pragma unroll
-  for (int i = 0; i < RPT; ++i)
-    if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
+  write_keep<NT, RPT>(kept, pos, budget, row0, sh, put);
 }
 
 // ---------------------------------------------------------------- Uniform Select
@@ -399,6 +444,7 @@ __device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_
     for (int32_t h = 0; h < heads; ++h) keep[(int64_t)h * budget + j] = row;
   };
 
+  neutral_missing_waves<NT>(sh);
   uint32_t fr[RPT];
   load_row_run<RPT, VEC>(frame_idx + base, S, row0, fr);
   const __amdgpu_buffer_rsrc_t frs = buffer_rsrc(frame_idx + base, (uint32_t)(S * 4));
@@ -433,7 +479,7 @@ __device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_
   const int32_t n_recent = n - n_past;
   if (any_bad || n_recent > budget) {
     if (tid == 0) raise_error(err, any_bad ? 2u : 4u);
-    for (int32_t j = tid; j < budget; j += NT) put(j, j);
+    for (int32_t j = tid; j < budget; j += (int32_t)blockDim.x) put(j, j);
     return;
   }
   const uint64_t past = valid & ~recent;
@@ -472,9 +518,7 @@ __device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_
   const uint64_t kept = recent | pick;
   int32_t total;
   int32_t pos = block_exclusive_scan<NT>(__popcll(kept), sh.wave_tot[2], &total);
-#pragma unroll
-  for (int i = 0; i < RPT; ++i)
-    if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
+  write_keep<NT, RPT>(kept, pos, budget, row0, sh, put);
 }
 
 // grid: one block per group of `heads` consecutive slices (heads > 1: every
