@@ -41,6 +41,10 @@
  * frames and is only ever compacted by this library (compaction is stable).
  * The recent window is every row whose frame id is >= F - r + 1, where F is
  * the frame id of row n-1 (a partial last frame counts as a frame).
+ * Scores accumulate in fp32: a K or V row's squared norm must lie in the
+ * fp32 range (finite, and normal unless the row is zero): element magnitudes
+ * up to about 1e18 for D = 128. A larger row has an infinite norm (its TaR is
+ * 0 and its VaN infinite); a smaller one loses precision.
  *
  * Pointer alignment: K, V, tar, van, frame_idx, patch_idx, keep_idx 16 bytes;
  * the workspace 256 bytes.
