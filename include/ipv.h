@@ -43,8 +43,9 @@
  * the frame id of row n-1 (a partial last frame counts as a frame).
  * Scores accumulate in fp32: a K or V row's squared norm must lie in the
  * fp32 range (finite, and normal unless the row is zero): element magnitudes
- * up to about 1e18 for D = 128. A larger row has an infinite norm (its TaR is
- * 0 and its VaN infinite); a smaller one loses precision.
+ * up to about 1e18 for D = 128. Beyond that the norm overflows and the
+ * scores that involve the row are not meaningful; below it precision is
+ * lost.
  *
  * Pointer alignment: K, V, tar, van, frame_idx, patch_idx, keep_idx 16 bytes;
  * the workspace 256 bytes.
