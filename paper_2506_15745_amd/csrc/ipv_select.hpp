@@ -195,11 +195,10 @@ __device__ __forceinline__ void block_min_max(const uint32_t (&key)[RPT], uint64
     sh.late_max[w] = mx;
   }
   __syncthreads();
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    mn = min(mn, sh.late_min[i]);
-    mx = max(mx, sh.late_max[i]);
-  }
+  // lane i reads wave i's range, a wave reduction combines them
+  mn = lane < NW ? sh.late_min[lane] : 0xffffffffu;
+  mx = lane < NW ? sh.late_max[lane] : 0u;
+  wave_min_max(mn, mx);
 }
 
 // Rows [row0, row0 + RPT) of one slice's column (S rows of 4 bytes); rows at
@@ -366,14 +365,14 @@ __device__ __forceinline__ void select_slice(const float* __restrict__ tar, cons
   }
   __syncthreads();
   bool any_bad = false;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    tmn = min(tmn, sh.wave_min[0][i]);
-    tmx = max(tmx, sh.wave_max[0][i]);
-    vmn = min(vmn, sh.wave_min[1][i]);
-    vmx = max(vmx, sh.wave_max[1][i]);
-    any_bad |= sh.wave_bad[i] != 0;
-  }
+  // lane i reads wave i's ranges, wave reductions combine them
+  tmn = lane < NW ? sh.wave_min[0][lane] : 0xffffffffu;
+  tmx = lane < NW ? sh.wave_max[0][lane] : 0u;
+  vmn = lane < NW ? sh.wave_min[1][lane] : 0xffffffffu;
+  vmx = lane < NW ? sh.wave_max[1][lane] : 0u;
+  wave_min_max(tmn, tmx);
+  wave_min_max(vmn, vmx);
+  any_bad = __ballot(lane < NW && sh.wave_bad[lane] != 0) != 0;
   // with non-decreasing frame ids the window is the suffix starting at first_recent
   const int32_t n_recent = n - sh.first_recent;
   const bool broken = any_bad || n_recent > budget;
