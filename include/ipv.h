@@ -104,7 +104,7 @@ enum {
   IPV_DEV_RECENT_OVER = 4u,    /* recent window |R| larger than the budget: keep_idx set to 0..C-1 (the
                                   compaction then moves nothing) */
   IPV_DEV_BAD_KEEP = 8u,       /* keep_idx[j] outside [j, n) or not above keep_idx[j-1]: the compaction
-                                  chunk (256 rows) holding row j was not moved */
+                                  chunk (512 rows) holding row j was not moved */
   IPV_DEV_NAN = 16u,           /* a candidate score is NaN: its rank is unspecified */
   IPV_DEV_WAIT_TIMEOUT = 32u   /* compaction: a chunk's bounded wait expired or its walk's counters were
                                   not zero (a workspace shared by overlapping calls); its rows were not
@@ -204,7 +204,7 @@ ipv_status ipv_select(const ipv_shape* shape, const float* tar, const float* van
  * In-place compaction (Sec. 3.1; Algorithm 1 step (5)): for j < C, row j of
  * K, V, frame_idx and patch_idx becomes a bit copy of row keep_idx[j]. Each
  * slice's keep_idx must be strictly ascending with entries in [0, n) (so
- * keep_idx[j] >= j), as ipv_select writes it; a chunk of 256 rows holding an
+ * keep_idx[j] >= j), as ipv_select writes it; a chunk of 512 rows holding an
  * entry that breaks this is not moved and raises IPV_DEV_BAD_KEEP. Rows
  * [C, S) are left unspecified and free for new frames. The caller then sets
  * n_tokens[b] = C for every stream with n_tokens[b] > 0.

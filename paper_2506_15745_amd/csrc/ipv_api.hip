@@ -28,8 +28,8 @@ constexpr int32_t kMaxRows = 65536;  // select: 1024 threads x 64 row flags
 constexpr int64_t kMaxWindowRows = 65536;        // r * p: recent rows scanned per table block
 constexpr int32_t kMaxRecentFrames = 256;
 static_assert(kPrevMaxPositions >= kPoolCells, "the prev-row walk holds one entry per patch position");
-constexpr int kCompactThreads = 512;
-constexpr int kCompactRows = 256;      // rows per compaction chunk
+constexpr int kCompactThreads = 1024;
+constexpr int kCompactRows = 512;      // rows per compaction chunk
 constexpr int kCompactColBytes = 256;  // largest column block a compaction walk copies
 
 struct Dims {
