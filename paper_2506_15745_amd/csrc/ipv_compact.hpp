@@ -140,8 +140,9 @@ __device__ __forceinline__ void compact_walk(char* __restrict__ K, char* __restr
         const int64_t j = c0 + u * RPS + sub;
         const int32_t s = kj[u];
         src[u] = (j < c1 && s > j && s < n) ? s : -1;
-        const auto v =
-            __builtin_amdgcn_raw_buffer_load_b128(drs, src[u] >= 0 ? (uint32_t)src[u] * RB + col : kSkip, 0, 0);
+        // nontemporal: the pass reads each kept row once here and not again
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(drs, src[u] >= 0 ? (uint32_t)src[u] * RB + col : kSkip,
+                                                             0, kNontemporal);
         buf[u].w[0] = v[0];
         buf[u].w[1] = v[1];
         buf[u].w[2] = v[2];

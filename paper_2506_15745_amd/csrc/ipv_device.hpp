@@ -77,6 +77,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferDword3);
 }
 
+// Cache-policy operand of a buffer load that streams data read once
+// (gfx950 encoding of the nontemporal bit).
+constexpr int kNontemporal = 2;
+
 // Nontemporal (streaming) store: compacted rows are not read again in the
 // pass, and storing them this way keeps them from lingering as dirty lines
 // that a later kernel's reads would have to write back first.

@@ -255,7 +255,8 @@ __device__ __forceinline__ void sweep_tile(const T* __restrict__ K, const T* __r
   for (int u = 0; u < U; ++u) {
     const uint32_t x = (f0 + u) * p + col;
     if (TAR) {
-      const auto k = __builtin_amdgcn_raw_buffer_load_b128(krs, x < past_end ? x * RB + lo : kSkip, 0, 0);
+      // nontemporal: each past key is read once by the pass's scoring
+      const auto k = __builtin_amdgcn_raw_buffer_load_b128(krs, x < past_end ? x * RB + lo : kSkip, 0, kNontemporal);
       kr[u].w[0] = k[0];
       kr[u].w[1] = k[1];
       kr[u].w[2] = k[2];
