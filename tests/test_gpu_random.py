@@ -48,7 +48,7 @@ def draw(seed):
                 alpha=alpha, mode=mode, tau=tau)
 
 
-@pytest.mark.parametrize("seed", range(256))
+@pytest.mark.parametrize("seed", range(1024))
 def test_random_configuration(seed):
     c = draw(seed)
     print("draw", seed, c, flush=True)
