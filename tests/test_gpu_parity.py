@@ -255,3 +255,27 @@ def test_nan_scores_are_reported_and_the_pass_stays_well_formed():
     n_recent = w.recent_frames * w.p
     assert np.all(got.keep[..., -n_recent:] == np.arange(w.n_tokens - n_recent, w.n_tokens, dtype=np.int32))
     P.oracle_gather_equal(K, V, fr, pa, w.n_tokens, got.keep, got)
+
+
+@pytest.mark.parametrize("C", [1, 511, 512, 513, 1024, 1025, 1999])
+def test_compaction_at_chunk_boundaries(C):
+    # keep sets whose size falls on, just below and just above the compaction's
+    # chunk boundaries (512 rows), with sources spread over the whole slice
+    from paper_2506_15745_amd import ipv
+    rng = np.random.default_rng(91 + C)
+    B, L, H, n, S, D = 1, 2, 2, 2000, 2003, 128
+    K = rng.integers(0, 2**15, size=(B, L, H, S, D)).astype(np.uint16)
+    V = rng.integers(0, 2**15, size=(B, L, H, S, D)).astype(np.uint16)
+    fr = np.tile(np.arange(S, dtype=np.int32), (B, L, H, 1))
+    pa = fr + 5000
+    keep1 = np.sort(rng.choice(n, C, replace=False)).astype(np.int32)
+    keep = np.ascontiguousarray(np.broadcast_to(keep1, (B, L, H, C)))
+    Kd, Vd, fd, pd = P.to_device(K, "bf16"), P.to_device(V, "bf16"), P.to_device(fr), P.to_device(pa)
+    ws = ipv.alloc_workspace(ipv.shape_of(Kd, 1, 1), "cuda:0")
+    ipv.ipv_compact(Kd, Vd, fd, pd, n, P.to_device(keep), C, ws, 1, 1)
+    torch.cuda.synchronize()
+    assert ipv.ipv_read_device_errors(ws) == 0
+    Kh, Vh, fh, ph = P.to_host(Kd), P.to_host(Vd), P.to_host(fd), P.to_host(pd)
+    assert np.array_equal(Kh[..., :C, :], K[..., keep1, :]) and np.array_equal(Vh[..., :C, :], V[..., keep1, :])
+    assert np.array_equal(fh[..., :C], fr[..., keep1]) and np.array_equal(ph[..., :C], pa[..., keep1])
+    assert np.array_equal(Kh[..., n:, :], K[..., n:, :])
