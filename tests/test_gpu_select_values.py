@@ -54,3 +54,29 @@ def test_selection_on_extreme_score_values(kind, mode):
         torch.cuda.synchronize()
         assert ipv.ipv_read_device_errors(ws) == 0
         assert np.array_equal(keep.cpu().numpy(), sel.keep_idx), (kind, mode, budget, alpha)
+
+
+@pytest.mark.parametrize("n", [1, 63, 64, 65, 256, 257, 4096, 4097, 6272, 8192, 8193, 16385, 65536])
+def test_selection_workgroup_sizes(n):
+    """The selection's workgroup is fitted to the rows (whole waves for n rows
+    at 4, 8, 16, 32 or 64 rows a thread): counts on both sides of each step
+    give the oracle's keep sets."""
+    from paper_2506_15745_amd import ipv
+    rng = np.random.default_rng(n)
+    B, L, H, gh, gw, r = 1, 1, 2, 1, 1, 1
+    S = n + (n % 3)
+    fr = np.full((B, L, H, S), -1, np.int32)
+    fr[..., :n] = np.arange(n, dtype=np.int32)  # one row per frame: the window is the last row
+    tar = rng.standard_normal((B, L, H, S)).astype(np.float32)
+    van = np.abs(rng.standard_normal((B, L, H, S))).astype(np.float32)
+    tar[..., ::7] = 0.5  # ties
+    for budget, alpha in ((max(1, n // 2), 0.5), (n, 0.5), (1, 0.0)):
+        print("case n=%d C=%d alpha=%s" % (n, budget, alpha), flush=True)
+        sel = oracle.select(tar, van, fr, n, budget, alpha, r)
+        keep = torch.zeros((B, L, H, budget), dtype=torch.int32, device="cuda:0")
+        ws = ipv.alloc_workspace(ipv.Shape(B, L, H, 64, S, gh, gw, 0), "cuda:0")
+        ipv.ipv_select(P.to_device(tar), P.to_device(van), P.to_device(fr), n, budget, alpha, r, keep, ws, gh, gw,
+                       head_dim=64)
+        torch.cuda.synchronize()
+        assert ipv.ipv_read_device_errors(ws) == 0
+        assert np.array_equal(keep.cpu().numpy(), sel.keep_idx), (n, budget, alpha)
