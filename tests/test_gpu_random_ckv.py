@@ -5,9 +5,11 @@ shape, grid, cap, budget (down to the largest recent window), TaR share,
 variant mode and pooling drawn at random; each case prints its draw."""
 import numpy as np
 import pytest
+import torch
 
 import synth
 from paper_2506_15745_amd import ipv
+from tests import parity as P
 from tests.test_gpu_ckv import run_loop
 
 pytestmark = pytest.mark.gpu
@@ -43,3 +45,83 @@ def test_random_ckv_loop(seed):
                       c["alpha"], c["dtype"], 11000 + seed, synth.RhoSpec(0.0, 0.99, 0.3), c["mode"], c["tau"],
                       c["sigma"])
     assert passes >= 1
+
+
+def draw_stream(seed):
+    rng = np.random.default_rng(8000 + seed)
+    dtype = synth.BF16 if rng.random() < 0.7 else synth.F32
+    D = int(rng.choice([32, 64, 128]))
+    gh, gw = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+    p = gh * gw
+    rows = p if rng.random() < 0.6 else int(rng.integers(1, p + 1))  # rows < p: every frame partial
+    B, L, H = int(rng.integers(1, 4)), int(rng.integers(1, 3)), int(rng.integers(1, 3))
+    r = int(rng.integers(1, 4))
+    # a pass needs budget >= min(len, r * p) whatever the frames hold
+    cap = r * p + int(rng.integers(1, 6)) * rows + int(rng.integers(0, rows))
+    budget = int(rng.integers(r * p, cap))
+    frames = int(rng.integers(1, 4 * (cap // rows) + 3))
+    start = [int(rng.integers(0, cap)) if rng.random() < 0.6 else 0 for _ in range(B)]
+    cuts = sorted(int(x) for x in rng.integers(0, frames + 1, size=int(rng.integers(0, 3))))
+    return dict(dtype=dtype, D=D, gh=gh, gw=gw, rows=rows, B=B, L=L, H=H, r=r, cap=cap, budget=budget,
+                frames=frames, start=start, cuts=cuts, alpha=float(rng.choice([0.0, 0.5, 1.0])),
+                mode=int(rng.choice(MODES)), tau=(0.3, 0.5, 0.7) if rng.random() < 0.3 else None)
+
+
+@pytest.mark.parametrize("seed", range(256))
+def test_random_ckv_stream_equals_step_by_step(seed):
+    """ipv_ckv_stream over the frames, cut into stretches at random points,
+    leaves the cache that one ipv_ckv_step per frame leaves, bit for bit."""
+    c = draw_stream(seed)
+    print("draw", seed, c, flush=True)
+    L, H, D, B, rows, cap = c["L"], c["H"], c["D"], c["B"], c["rows"], c["cap"]
+    p = c["gh"] * c["gw"]
+    S = cap + rows
+    kind = "bf16" if c["dtype"] == synth.BF16 else "raw"
+    tdt, bits = (torch.bfloat16, torch.int16) if c["dtype"] == synth.BF16 else (torch.float32, torch.int32)
+    F = c["frames"]
+    src = [synth.fresh_cache(12000 + 7 * seed + b, L, H, F * p, D, c["gh"], c["gw"], F * p, c["dtype"],
+                             synth.RhoSpec(0.0, 0.99, 0.3)) for b in range(B)]
+    fK = np.ascontiguousarray(np.stack([np.stack([s.K[:, :, f * p:f * p + rows] for s in src]) for f in range(F)]))
+    fV = np.ascontiguousarray(np.stack([np.stack([s.V[:, :, f * p:f * p + rows] for s in src]) for f in range(F)]))
+    fKd, fVd = P.to_device(fK, kind), P.to_device(fV, kind)
+    # rows already in the cache: whole frames of their own, ids below the stretch's
+    old = [synth.fresh_cache(13000 + 7 * seed + b, L, H, S, D, c["gh"], c["gw"], n, c["dtype"],
+                             synth.RhoSpec(0.0, 0.99, 0.3)) if n else None for b, n in enumerate(c["start"])]
+
+    def fresh():
+        K = torch.zeros((B, L, H, S, D), dtype=tdt, device="cuda:0")
+        V = torch.zeros_like(K)
+        fr = torch.full((B, L, H, S), -1, dtype=torch.int32, device="cuda:0")
+        pa = torch.full_like(fr, -1)
+        for b, st in enumerate(old):
+            n = c["start"][b]
+            if st is not None:
+                K[b, :, :, :n] = P.to_device(np.ascontiguousarray(st.K[:, :, :n]), kind)
+                V[b, :, :, :n] = P.to_device(np.ascontiguousarray(st.V[:, :, :n]), kind)
+                fr[b, :, :, :n] = P.to_device(np.ascontiguousarray(st.frame_idx[:, :, :n] - 1000))
+                pa[b, :, :, :n] = P.to_device(np.ascontiguousarray(st.patch_idx[:, :, :n]))
+        return K, V, fr, pa, ipv.Compressor(K, c["gh"], c["gw"], c["budget"])
+
+    args = (cap, c["budget"], c["alpha"], c["r"], c["tau"])
+    K1, V1, f1, p1, c1 = fresh()
+    n1, passes1 = list(c["start"]), [0] * B
+    for f in range(F):
+        n1, fired = ipv.ipv_ckv_step(K1, V1, f1, p1, n1, fKd[f], fVd[f], f, 0, *args, c1.tar, c1.van, c1.keep_idx,
+                                     c1.ws, c["gh"], c["gw"], mode=c["mode"])
+        passes1 = [a + int(x) for a, x in zip(passes1, fired)]
+    K2, V2, f2, p2, c2 = fresh()
+    n2, passes2 = list(c["start"]), [0] * B
+    for a, b in zip([0] + c["cuts"], c["cuts"] + [F]):
+        if b > a:
+            n2, ps = ipv.ipv_ckv_stream(K2, V2, f2, p2, n2, fKd[a:b], fVd[a:b], a, *args, c2.tar, c2.van,
+                                        c2.keep_idx, c2.ws, c["gh"], c["gw"], mode=c["mode"])
+            passes2 = [x + y for x, y in zip(passes2, ps)]
+    torch.cuda.synchronize()
+    assert c1.device_errors() == 0 and c2.device_errors() == 0
+    assert n2 == n1 and passes2 == passes1
+    for b in range(B):
+        m = n1[b]
+        assert torch.equal(K1[b, :, :, :m].view(bits), K2[b, :, :, :m].view(bits))
+        assert torch.equal(V1[b, :, :, :m].view(bits), V2[b, :, :, :m].view(bits))
+        assert torch.equal(f1[b, :, :, :m], f2[b, :, :, :m]) and torch.equal(p1[b, :, :, :m], p2[b, :, :, :m])
+    print("passes per stream %s, final rows %s" % (passes1, n1), flush=True)
