@@ -291,28 +291,34 @@ ipv_status run_select(const Dims& d, const float* tar, const float* van, const i
   return launched();
 }
 
-// Uniform Select: one block per slice, or per (stream, layer) with IPV_HEAD_SHARED
+// Uniform Select: one block per slice, or per (stream, layer) with
+// IPV_HEAD_SHARED. zero (may be null): the blocks also zero zero_per_slice
+// words per slice there (the compaction flags of the pass).
 template <int RPT>
 ipv_status run_uniform(const Dims& d, const int32_t* fr, int32_t n, int32_t budget, int32_t r, int32_t* keep,
-                       uint32_t* err, hipStream_t st, uint32_t mode) {
+                       uint32_t* err, hipStream_t st, uint32_t mode, uint32_t* zero, int32_t zero_per_slice) {
   const int32_t heads = (mode & IPV_HEAD_SHARED) ? (int32_t)d.H : 1;
   const dim3 grid((uint32_t)(d.slices / heads)), block(sel_threads(n, RPT));
   if (d.S % 4 == 0)
-    k_select_uniform<kSelThreads, RPT, true><<<grid, block, 0, st>>>(fr, d.S, n, budget, r, keep, err, heads);
+    k_select_uniform<kSelThreads, RPT, true><<<grid, block, 0, st>>>(fr, d.S, n, budget, r, keep, err, heads, zero,
+                                                                     zero_per_slice);
   else
-    k_select_uniform<kSelThreads, RPT, false><<<grid, block, 0, st>>>(fr, d.S, n, budget, r, keep, err, heads);
+    k_select_uniform<kSelThreads, RPT, false><<<grid, block, 0, st>>>(fr, d.S, n, budget, r, keep, err, heads, zero,
+                                                                      zero_per_slice);
   return launched();
 }
 
+// zero / zero_per_slice: as for run_uniform (used by Uniform Select only)
 ipv_status select(const Dims& d, const float* tar, const float* van, const int32_t* fr, int32_t n, int32_t budget,
-                  int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st, uint32_t mode) {
+                  int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st, uint32_t mode,
+                  uint32_t* zero = nullptr, int32_t zero_per_slice = 0) {
   const int32_t rpt = (n + kSelThreads - 1) / kSelThreads;
   if (mode & IPV_UNIFORM_SELECT) {
-    if (rpt <= 4) return run_uniform<4>(d, fr, n, budget, r, keep, err, st, mode);
-    if (rpt <= 8) return run_uniform<8>(d, fr, n, budget, r, keep, err, st, mode);
-    if (rpt <= 16) return run_uniform<16>(d, fr, n, budget, r, keep, err, st, mode);
-    if (rpt <= 32) return run_uniform<32>(d, fr, n, budget, r, keep, err, st, mode);
-    return run_uniform<64>(d, fr, n, budget, r, keep, err, st, mode);
+    if (rpt <= 4) return run_uniform<4>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
+    if (rpt <= 8) return run_uniform<8>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
+    if (rpt <= 16) return run_uniform<16>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
+    if (rpt <= 32) return run_uniform<32>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
+    return run_uniform<64>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
   }
   if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
@@ -474,10 +480,12 @@ ipv_status compress_run(const Dims& d, void* K, void* V, int32_t* fr, int32_t* p
   IPV_TRY(mark(2));
   if (cv_tau && !uniform) IPV_TRY(pool_d(d, cv_tau, van, fr, pa, n, nullptr, ws, st));
   IPV_TRY(mark(3));
-  IPV_TRY(select(d, tar, van, fr, n, budget, floor_share(alpha, budget), r, keep, err_word(ws), st, mode));
+  // the score launches zero the compaction's flags; without them the uniform selection does
+  IPV_TRY(select(d, tar, van, fr, n, budget, floor_share(alpha, budget), r, keep, err_word(ws), st, mode,
+                 uniform ? ws_flags(ws, d) : nullptr,
+                 (int32_t)(compact_parts(d) * walk_words(compact_chunks(budget)))));
   IPV_TRY(mark(4));
-  // the score launches zero the compaction's flags; without them the compaction does
-  IPV_TRY(compact(d, K, V, fr, pa, n, keep, budget, ws, st, !uniform));
+  IPV_TRY(compact(d, K, V, fr, pa, n, keep, budget, ws, st, true));
   return mark(5);
 }
 

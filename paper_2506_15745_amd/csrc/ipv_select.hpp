@@ -433,7 +433,8 @@ __device__ __forceinline__ bool uniform_taken(int64_t rank, int64_t k, int64_t q
 template <int NT, int RPT, bool VEC>
 __device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
                                               int32_t budget, int32_t r, int32_t* __restrict__ keep_idx,
-                                              uint32_t* err, int64_t slice, int32_t heads, SelShared<NT>& sh) {
+                                              uint32_t* err, int64_t slice, int32_t heads, uint32_t* __restrict__ zero,
+                                              int32_t zero_per_slice, SelShared<NT>& sh) {
   constexpr int NW = NT / kWave;
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int64_t base = slice * S;
@@ -442,6 +443,11 @@ __device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_
   auto put = [&](int32_t j, int32_t row) {
     for (int32_t h = 0; h < heads; ++h) keep[(int64_t)h * budget + j] = row;
   };
+  // no score kernel runs before this selection in a pass: it zeroes the
+  // compaction flags of its slices (zero_per_slice words each) instead
+  if (zero)
+    for (int64_t i = tid; i < (int64_t)heads * zero_per_slice; i += (int64_t)blockDim.x)
+      zero[slice * zero_per_slice + i] = 0u;
 
   neutral_missing_waves<NT>(sh);
   uint32_t fr[RPT];
@@ -521,13 +527,16 @@ __device__ __forceinline__ void uniform_slice(const int32_t* __restrict__ frame_
 }
 
 // grid: one block per group of `heads` consecutive slices (heads > 1: every
-// head must hold the same frame ids and receives the same keep set)
+// head must hold the same frame ids and receives the same keep set).
+// zero (may be null): zero_per_slice words per slice to clear
 template <int NT, int RPT, bool VEC>
 __global__ __launch_bounds__(NT) void k_select_uniform(const int32_t* __restrict__ frame_idx, int64_t S, int32_t n,
                                                        int32_t budget, int32_t r, int32_t* __restrict__ keep_idx,
-                                                       uint32_t* err, int32_t heads) {
+                                                       uint32_t* err, int32_t heads, uint32_t* __restrict__ zero,
+                                                       int32_t zero_per_slice) {
   __shared__ SelShared<NT> sh;
-  uniform_slice<NT, RPT, VEC>(frame_idx, S, n, budget, r, keep_idx, err, (int64_t)blockIdx.x * heads, heads, sh);
+  uniform_slice<NT, RPT, VEC>(frame_idx, S, n, budget, r, keep_idx, err, (int64_t)blockIdx.x * heads, heads, zero,
+                              zero_per_slice, sh);
 }
 
 // grid: one block per group of `heads` consecutive slices
