@@ -329,7 +329,8 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
 
 int64_t compact_chunks(int32_t budget) { return (budget + kCompactRows - 1) / kCompactRows; }
 
-// flags_zeroed: the pass's table kernel has zeroed the flags already
+// flags_zeroed: an earlier kernel of the pass (the table or prev-row launch, or
+// the uniform selection) has zeroed the flags already
 template <int RB>
 ipv_status run_compact(const Dims& d, void* K, void* V, int32_t* fr, int32_t* pa, int32_t n, const int32_t* keep,
                        int32_t budget, void* ws, hipStream_t st, bool flags_zeroed) {

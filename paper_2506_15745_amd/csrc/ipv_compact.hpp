@@ -34,7 +34,8 @@
 //
 // Per walk the workspace holds one flag per chunk and then the ticket
 // counter, all zero when the kernel starts; k_clear_flags (or, in a full
-// pass, the table kernel) zeroes them.
+// pass, the first kernel: the table or prev-row launch, or the Uniform Select
+// selection) zeroes them.
 #pragma once
 
 #include "ipv_device.hpp"
