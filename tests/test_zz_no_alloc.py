@@ -3,7 +3,8 @@
 Its results must equal ipv_compress's on the same inputs (same kernels), and
 match the oracle by the usual rule. Two calls in a row with different shapes,
 the second smaller, check that what the first call left in the shared
-workspace does not leak into the second; a third repeats the first.
+workspace does not leak into the second; a third repeats the first, and
+Uniform Select calls (whose selection zeroes the compaction flags) follow.
 """
 import numpy as np
 import pytest
@@ -33,14 +34,28 @@ def noalloc_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, tau=None, mode=0):
                      P.to_host(pd), int(err.item()))
 
 
+def compress_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, tau=None, mode=0):
+    """The same pass through ipv_compress with a workspace of its own."""
+    if mode == 0:
+        return P.gpu_compress(K, V, fr, pa, n, budget, alpha, r, gh, gw, tau)
+    kind = "bf16" if K.dtype == np.uint16 else "raw"
+    Kd, Vd, fd, pd = P.to_device(K, kind), P.to_device(V, kind), P.to_device(fr), P.to_device(pa)
+    comp = ipv.Compressor(Kd, gh, gw, budget)
+    comp.compress(Kd, Vd, fd, pd, n, alpha, r, tau, mode=mode)
+    torch.cuda.synchronize()
+    return P.GpuPass(P.to_host(comp.tar), P.to_host(comp.van), P.to_host(comp.keep_idx), P.to_host(Kd),
+                     P.to_host(Vd), P.to_host(fd), P.to_host(pd), comp.device_errors())
+
+
 def check_against_compress(name, K, V, fr, pa, n, budget, alpha, r, gh, gw, tau=None, mode=0):
-    print("case", name, K.shape, n, budget, alpha, flush=True)
+    print("case", name, K.shape, n, budget, alpha, mode, flush=True)
     got = noalloc_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, tau, mode)
-    ref = P.gpu_compress(K, V, fr, pa, n, budget, alpha, r, gh, gw, tau)
+    ref = compress_pass(K, V, fr, pa, n, budget, alpha, r, gh, gw, tau, mode)
     assert got.errors == 0 and ref.errors == 0
     # the same kernels on the same inputs: identical scores, keep sets and cache
-    assert np.array_equal(got.tar[..., :n].view(np.uint32), ref.tar[..., :n].view(np.uint32))
-    assert np.array_equal(got.van[..., :n].view(np.uint32), ref.van[..., :n].view(np.uint32))
+    if not mode & ipv.UNIFORM_SELECT:  # Uniform Select writes no scores
+        assert np.array_equal(got.tar[..., :n].view(np.uint32), ref.tar[..., :n].view(np.uint32))
+        assert np.array_equal(got.van[..., :n].view(np.uint32), ref.van[..., :n].view(np.uint32))
     assert np.array_equal(got.keep, ref.keep)
     C = budget
     for a, b in ((got.K, ref.K), (got.V, ref.V), (got.frame_idx, ref.frame_idx), (got.patch_idx, ref.patch_idx)):
@@ -63,6 +78,14 @@ def test_noalloc_equals_compress_on_consecutive_calls():
     check_against_compress("tiny", *cache_of(t), t.n_tokens, t.budget, 0.5, t.recent_frames, t.grid_h, t.grid_w)
     check_against_compress("7b-class again", K, V, fr, pa, w.n_tokens, w.budget, 0.5, w.recent_frames, w.grid_h,
                            w.grid_w)
+    # Uniform Select runs no score kernel, so its selection zeroes the compaction's
+    # flags and tickets, which the calls before left set in the shared workspace
+    check_against_compress("7b-class, Uniform Select", K, V, fr, pa, w.n_tokens, w.budget, 0.5, w.recent_frames,
+                           w.grid_h, w.grid_w, mode=ipv.UNIFORM_SELECT)
+    check_against_compress("7b-class, 5 layers, 3000 rows, Uniform Select, heads shared", k2, v2, f2, p2, n, 1700,
+                           0.6, w.recent_frames, w.grid_h, w.grid_w, mode=ipv.UNIFORM_SELECT | ipv.HEAD_SHARED)
+    check_against_compress("7b-class after Uniform Select", K, V, fr, pa, w.n_tokens, w.budget, 0.5,
+                           w.recent_frames, w.grid_h, w.grid_w)
 
 
 def test_noalloc_reports_device_errors():
