@@ -251,10 +251,11 @@ ipv_status scores(const Dims& d, const void* K, const void* V, const int32_t* fr
 
 ipv_status pool_d(const Dims& d, const double* tau, float* van, const int32_t* fr, const int32_t* pa, int32_t n,
                   int32_t* pool_out, void* ws, hipStream_t st) {
-  k_pool_cv<<<dim3((uint32_t)(d.B * d.L)), dim3(256), 0, st>>>(van, d.S, n, (int32_t)d.H, tau[0], tau[1], tau[2],
-                                                               ws_pool(ws, d), pool_out);
-  k_pool_apply<<<dim3((uint32_t)d.slices), dim3(256), 0, st>>>(van, fr, pa, d.S, n, (int32_t)d.H, d.gh, d.gw,
-                                                               ws_pool(ws, d));
+  k_pool_cv<<<dim3((uint32_t)(d.B * d.L)), dim3(kPoolThreads), 0, st>>>(van, d.S, n, (int32_t)d.H, tau[0], tau[1],
+                                                                        tau[2], ws_pool(ws, d), pool_out);
+  k_pool_apply<<<dim3((uint32_t)d.slices), dim3(kPoolThreads), 0, st>>>(
+      van, fr, pa, d.S, n, (int32_t)d.H, d.gh, d.gw, ws_pool(ws, d), make_fastdiv((uint32_t)d.p),
+      make_fastdiv((uint32_t)d.gw));
   return launched();
 }
 

@@ -413,39 +413,74 @@ __global__ __launch_bounds__(256) void k_table_van(const T* __restrict__ K, cons
 }
 
 // ---------------------------------------------------------------- adaptive pooling
+// Both kernels run kPoolThreads threads a workgroup; a thread takes rows
+// tid, tid + kPoolThreads, ... and issues kPoolBatch of their loads at once
+// (buffer loads: rows past n read as zero and are left out).
+constexpr int kPoolThreads = 1024;
+constexpr int kPoolBatch = 8;
+constexpr int kPoolHeads = 4;  // the CV loads this many heads' rows at once
+
+// Sum over the workgroup in a fixed order: a butterfly inside each wave, then
+// the wave totals in wave order. Every thread gets the sum. red: one slot per
+// wave, free again when this returns.
+__device__ __forceinline__ double pool_block_sum(double v, double* red) {
+  constexpr int NW = kPoolThreads / kWave;
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off /= 2) v += __shfl_xor(v, off);
+  if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = v;
+  __syncthreads();
+  double t = 0.0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) t += red[i];
+  __syncthreads();
+  return t;
+}
+
 // Per (stream, layer): CV of all H * n VaN values in fp64, two passes (mean,
-// then squared deviations), fixed-order reduction; window k from the
+// then squared deviations), each a fixed-order reduction; window k from the
 // thresholds. One workgroup per (stream, layer).
-__global__ __launch_bounds__(256) void k_pool_cv(const float* __restrict__ van, int64_t S, int32_t n, int32_t H,
-                                                 double tau1, double tau2, double tau3,
-                                                 int32_t* __restrict__ pool_ws, int32_t* __restrict__ pool_out) {
-  __shared__ double red[256];
+__global__ __launch_bounds__(kPoolThreads) void k_pool_cv(const float* __restrict__ van, int64_t S, int32_t n,
+                                                          int32_t H, double tau1, double tau2, double tau3,
+                                                          int32_t* __restrict__ pool_ws,
+                                                          int32_t* __restrict__ pool_out) {
+  constexpr int NT = kPoolThreads, U = kPoolBatch;
+  __shared__ double red[NT / kWave];
   const int tid = threadIdx.x;
   const int64_t bl = blockIdx.x;
-  const int64_t count = (int64_t)H * n;
-  double s = 0.0;
-  for (int64_t i = tid; i < count; i += 256) s += (double)van[(bl * H + i / n) * S + i % n];
-  red[tid] = s;
-  __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if (tid < w) red[tid] += red[tid + w];
-    __syncthreads();
-  }
-  const double mean = red[0] / (double)count;
-  __syncthreads();
-  double v = 0.0;
-  for (int64_t i = tid; i < count; i += 256) {
-    const double d = (double)van[(bl * H + i / n) * S + i % n] - mean;
-    v += d * d;
-  }
-  red[tid] = v;
-  __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if (tid < w) red[tid] += red[tid + w];
-    __syncthreads();
-  }
+  const double count = (double)H * (double)n;
+  // Pass `second`: the sum of the values, else of their squared deviations
+  // from `mean`. Loads go out kPoolHeads heads x kPoolBatch rows at a time
+  // (a missing head reads from an empty resource: zeros, left out).
+  auto sweep = [&](bool second, double mean) -> double {
+    double acc = 0.0;
+    for (int32_t h0 = 0; h0 < H; h0 += kPoolHeads) {
+      __amdgpu_buffer_rsrc_t rs[kPoolHeads];
+#pragma unroll
+      for (int g = 0; g < kPoolHeads; ++g)
+        rs[g] = buffer_rsrc(van + (bl * H + min(h0 + g, H - 1)) * S, h0 + g < H ? (uint32_t)n * 4u : 0u);
+      for (int32_t x0 = tid; x0 < n; x0 += NT * U) {
+        float t[kPoolHeads][U];
+#pragma unroll
+        for (int g = 0; g < kPoolHeads; ++g)
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            t[g][u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs[g], (uint32_t)(x0 + u * NT) * 4u, 0, 0));
+#pragma unroll
+        for (int g = 0; g < kPoolHeads; ++g)
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            if (h0 + g < H && x0 + u * NT < n) {
+              const double d = second ? (double)t[g][u] - mean : (double)t[g][u];
+              acc += second ? d * d : d;
+            }
+      }
+    }
+    return acc;
+  };
+  const double mean = pool_block_sum(sweep(false, 0.0), red) / count;
+  const double v = sweep(true, mean);
+  const double sd = sqrt(pool_block_sum(v, red) / count);
   if (tid == 0) {
-    const double sd = sqrt(red[0] / (double)count);
     const double cv = mean == 0.0 ? 0.0 : sd / mean;
     const int32_t k = cv < tau1 ? 7 : cv < tau2 ? 5 : cv < tau3 ? 3 : 1;
     pool_ws[bl] = k;
@@ -453,65 +488,177 @@ __global__ __launch_bounds__(256) void k_pool_cv(const float* __restrict__ van, 
   }
 }
 
+// The k x k window mean is separable: every cell first gets the sum and count
+// of the present cells (value >= 0) in its row of the window (hsum, hcnt),
+// then a row adds those of the window's rows, top to bottom. Cells outside
+// the grid are masked (a masked term adds exactly +0).
+template <int HALF>
+__device__ __forceinline__ void window_row(const float* cell, float* hsum, uint8_t* hcnt, int32_t c, int32_t p,
+                                           int32_t grid_w, const FastDiv& pdiv, const FastDiv& wdiv) {
+  const int32_t qq = c - (int32_t)fast_div((uint32_t)c, pdiv) * p;
+  const int32_t cj = qq - (int32_t)fast_div((uint32_t)qq, wdiv) * grid_w, row0 = c - cj;
+  float sum = 0.f;
+  int cnt = 0;
+#pragma unroll
+  for (int dj = -HALF; dj <= HALF; ++dj) {
+    const int32_t j = cj + dj;
+    const bool inside = (uint32_t)j < (uint32_t)grid_w;
+    const float v = cell[inside ? row0 + j : c];
+    const bool use = inside && v >= 0.f;
+    sum += use ? v : 0.f;
+    cnt += use;
+  }
+  hsum[c] = sum;
+  hcnt[c] = (uint8_t)cnt;
+}
+
+template <int HALF>
+__device__ __forceinline__ float window_col(const float* hsum, const uint8_t* hcnt, int32_t fo, int32_t q, int32_t p,
+                                            int32_t grid_h, int32_t grid_w, const FastDiv& wdiv) {
+  const int32_t ci = (int32_t)fast_div((uint32_t)q, wdiv), c = fo * p + q;
+  float sum = 0.f;
+  int cnt = 0;
+#pragma unroll
+  for (int di = -HALF; di <= HALF; ++di) {
+    const int32_t i = ci + di;
+    const bool inside = (uint32_t)i < (uint32_t)grid_h;
+    const int32_t at = inside ? c + di * grid_w : c;
+    sum += inside ? hsum[at] : 0.f;
+    cnt += inside ? hcnt[at] : 0;
+  }
+  return sum / (float)cnt;
+}
+
 // One workgroup per slice. Frames are handled FR at a time: their raw VaN
 // values are scattered into an LDS grid (absent cells hold -1), then every
-// row of those frames averages the present cells of its k x k window and
-// overwrites its own score. Rows of later frames still hold raw values. Each
+// row of those frames averages the present cells of its k x k window (the
+// separable sums above) and overwrites its own score. Rows of later frames still hold raw values. Each
 // round starts at the smallest frame id not yet covered, so the loop runs at
-// most once per present frame whatever the ids are.
+// most once per present frame whatever the ids are. Rows whose patch id is
+// outside the grid keep their raw value. A thread's first kPoolBatch rows
+// (all of them when n <= kPoolThreads * kPoolBatch) are loaded once and kept
+// in registers for every pass; later rows are loaded again in each pass.
 constexpr int kPoolCells = 8192;
 
-__global__ __launch_bounds__(256) void k_pool_apply(float* __restrict__ van, const int32_t* __restrict__ frame_idx,
-                                                    const int32_t* __restrict__ patch_idx, int64_t S, int32_t n,
-                                                    int32_t H, int32_t grid_h, int32_t grid_w,
-                                                    const int32_t* __restrict__ pool_ws) {
+__global__ __launch_bounds__(kPoolThreads) void k_pool_apply(float* __restrict__ van,
+                                                             const int32_t* __restrict__ frame_idx,
+                                                             const int32_t* __restrict__ patch_idx, int64_t S,
+                                                             int32_t n, int32_t H, int32_t grid_h, int32_t grid_w,
+                                                             const int32_t* __restrict__ pool_ws, FastDiv pdiv,
+                                                             FastDiv wdiv) {
+  constexpr int NT = kPoolThreads, U = kPoolBatch, NW = NT / kWave;
   __shared__ float cell[kPoolCells];
-  __shared__ int32_t next_frame;
+  __shared__ float hsum[kPoolCells];
+  __shared__ uint8_t hcnt[kPoolCells];
+  __shared__ int32_t wmin[NW];
+  __shared__ int32_t slots;  // frame slots of the round that hold a row
   const int tid = threadIdx.x;
   const int64_t slice = blockIdx.x;
   const int32_t k = pool_ws[slice / H];
-  if (k == 1) return;
-  const int32_t half = k / 2, p = grid_h * grid_w, FR = kPoolCells / p;
+  if (k != 3 && k != 5 && k != 7) return;  // 1: no pooling
+  const int32_t p = grid_h * grid_w, FR = kPoolCells / p;
   const int64_t base = slice * S;
-  int64_t lower = INT64_MIN;
-  for (;;) {
-    if (tid == 0) next_frame = INT32_MAX;
-    for (int i = tid; i < FR * p; i += 256) cell[i] = -1.f;
-    __syncthreads();
+  const __amdgpu_buffer_rsrc_t frs = buffer_rsrc(frame_idx + base, (uint32_t)n * 4u);
+  const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(patch_idx + base, (uint32_t)n * 4u);
+  const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(van + base, (uint32_t)n * 4u);
+  float* vcol = van + base;
+
+  int32_t f0[U], q0[U];
+  float v0[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint32_t off = (uint32_t)(tid + u * NT) * 4u;
+    f0[u] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, off, 0, 0);
+    q0[u] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, off, 0, 0);
+    v0[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(vrs, off, 0, 0));
+  }
+  // rows x0 + u * NT of batch b (b == 0: the registers above); rows past n read as 0
+  auto rows = [&](int32_t b, int32_t x0, int32_t (&f)[U], int32_t (&q)[U], float (&v)[U], bool need_v) {
+    if (b == 0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        f[u] = f0[u];
+        q[u] = q0[u];
+        v[u] = v0[u];
+      }
+      return;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t off = (uint32_t)(x0 + u * NT) * 4u;
+      f[u] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(frs, off, 0, 0);
+      q[u] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(prs, off, 0, 0);
+      v[u] = need_v ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(vrs, off, 0, 0)) : 0.f;
+    }
+  };
+
+  // the smallest frame id at or above `lower` (INT32_MAX: none); its barrier
+  // also ends every thread's use of `cell` before the next round clears it
+  auto next_start = [&](int64_t lower) -> int32_t {
     int32_t mine = INT32_MAX;
-    for (int64_t x = tid; x < n; x += 256) {
-      const int32_t f = frame_idx[base + x];
-      if ((int64_t)f >= lower && f < mine) mine = f;
+    for (int32_t b = 0, x0 = tid; x0 < n; ++b, x0 += NT * U) {
+      int32_t f[U], q[U];
+      float v[U];
+      rows(b, x0, f, q, v, false);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (x0 + u * NT < n && (int64_t)f[u] >= lower) mine = min(mine, f[u]);
     }
-    atomicMin(&next_frame, mine);
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off /= 2) mine = min(mine, __shfl_xor(mine, off));
+    if (tid % kWave == 0) wmin[tid / kWave] = mine;
     __syncthreads();
-    const int64_t fb = next_frame;
-    if (fb == INT32_MAX) break;
-    for (int64_t x = tid; x < n; x += 256) {
-      const int64_t fo = (int64_t)frame_idx[base + x] - fb;
-      const int32_t q = patch_idx[base + x];
-      if (fo >= 0 && fo < FR && q >= 0 && q < p) cell[fo * p + q] = van[base + x];
-    }
+    int32_t m = INT32_MAX;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) m = min(m, wmin[i]);
     __syncthreads();
-    for (int64_t x = tid; x < n; x += 256) {
-      const int64_t fo = (int64_t)frame_idx[base + x] - fb;
-      const int32_t q = patch_idx[base + x];
-      if (fo < 0 || fo >= FR || q < 0 || q >= p) continue;
-      const int32_t ci = q / grid_w, cj = q % grid_w;
-      float sum = 0.f;
-      int cnt = 0;
-      for (int32_t i = max(0, ci - half); i <= min(grid_h - 1, ci + half); ++i)
-        for (int32_t j = max(0, cj - half); j <= min(grid_w - 1, cj + half); ++j) {
-          const float c = cell[fo * p + i * grid_w + j];
-          if (c >= 0.f) {
-            sum += c;
-            ++cnt;
-          }
+    return m;
+  };
+
+  for (int32_t fb = next_start(INT64_MIN); fb != INT32_MAX; fb = next_start((int64_t)fb + FR)) {
+    for (int i = tid; i < FR * p; i += NT) cell[i] = -1.f;
+    if (tid == 0) slots = 0;
+    __syncthreads();
+    int32_t top = 0;  // 1 + the highest slot this thread fills
+    for (int32_t b = 0, x0 = tid; x0 < n; ++b, x0 += NT * U) {
+      int32_t f[U], q[U];
+      float v[U];
+      rows(b, x0, f, q, v, true);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t fo = (int64_t)f[u] - fb;
+        if (x0 + u * NT < n && fo >= 0 && fo < FR && q[u] >= 0 && q[u] < p) {
+          cell[fo * p + q[u]] = v[u];
+          top = max(top, (int32_t)fo + 1);
         }
-      van[base + x] = sum / (float)cnt;
+      }
     }
-    lower = fb + FR;
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off /= 2) top = max(top, __shfl_xor(top, off));
+    if (tid % kWave == 0) atomicMax(&slots, top);
     __syncthreads();
+    // window rows of the filled slots only
+    const int32_t cells = slots * p;
+    for (int c = tid; c < cells; c += NT) {
+      if (k == 7) window_row<3>(cell, hsum, hcnt, c, p, grid_w, pdiv, wdiv);
+      else if (k == 5) window_row<2>(cell, hsum, hcnt, c, p, grid_w, pdiv, wdiv);
+      else window_row<1>(cell, hsum, hcnt, c, p, grid_w, pdiv, wdiv);
+    }
+    __syncthreads();
+    for (int32_t b = 0, x0 = tid; x0 < n; ++b, x0 += NT * U) {
+      int32_t f[U], q[U];
+      float v[U];
+      rows(b, x0, f, q, v, false);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t fo = (int64_t)f[u] - fb;
+        if (x0 + u * NT >= n || fo < 0 || fo >= FR || q[u] < 0 || q[u] >= p) continue;
+        const int32_t slot = (int32_t)fo;
+        vcol[x0 + u * NT] = k == 7   ? window_col<3>(hsum, hcnt, slot, q[u], p, grid_h, grid_w, wdiv)
+                            : k == 5 ? window_col<2>(hsum, hcnt, slot, q[u], p, grid_h, grid_w, wdiv)
+                                     : window_col<1>(hsum, hcnt, slot, q[u], p, grid_h, grid_w, wdiv);
+      }
+    }
   }
 }
 
