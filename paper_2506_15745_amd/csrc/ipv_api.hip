@@ -159,10 +159,13 @@ ipv_status no_mark() { return IPV_OK; }
 // zero_chunks > 0: the first kernel also zeroes the compaction flags for a
 // compaction of zero_chunks chunks per walk that follows in the same pass.
 // adjacent: consecutive-frame TaR (IPV_TAR_ADJACENT)
+// cv_tau (may be null): with both scores and the recent-key table, the TaR
+// launch also computes the pooling CV and window of every (stream, layer)
+// (k_pool_apply must follow); ignored otherwise.
 template <typename T, int D, typename Between>
 ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
                       int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between,
-                      int64_t zero_chunks, bool adjacent) {
+                      int64_t zero_chunks, bool adjacent, const double* cv_tau) {
   const bool do_tar = K != nullptr, do_van = V != nullptr;
   uint32_t* zero = zero_chunks > 0 ? ws_flags(ws, d) : nullptr;
   const int32_t zero_per_slice = (int32_t)(compact_parts(d) * walk_words(zero_chunks));
@@ -212,6 +215,14 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
         k, v, fr, pa, d.S, n, r, (int32_t)d.p, blocks, table_padded, table_real, ws_table(ws), first, err_word(ws),
         zero, zero_per_slice, van, tile_grid(col_blocks, frame_blocks, work, pad8(work)));
     IPV_TRY(between());
+    if (cv_tau) {
+      const uint32_t cv_real = (uint32_t)(d.B * d.L), cv_padded = pad8(cv_real);
+      k_tar_sweep_cv<T, D><<<dim3(cv_padded + pad8(work)), block, 0, st>>>(
+          k, pa, d.S, n, (int32_t)d.p, ws_table(ws), first, tar, err_word(ws),
+          tile_grid(col_blocks, frame_blocks, work, pad8(work)), sure_past, van, (int32_t)d.H, cv_tau[0], cv_tau[1],
+          cv_tau[2], ws_pool(ws, d), cv_padded, cv_real);
+      return launched();
+    }
     k_score_sweep<T, D, true, false><<<grid, block, 0, st>>>(k, v, pa, d.S, n, (int32_t)d.p, ws_table(ws), first,
                                                              tar, van, err_word(ws),
                                                              tile_grid(col_blocks, frame_blocks, work, pad8(work)), sure_past);
@@ -236,10 +247,10 @@ ipv_status run_scores(const Dims& d, const void* K, const void* V, const int32_t
 template <typename Between = ipv_status (*)()>
 ipv_status scores(const Dims& d, const void* K, const void* V, const int32_t* fr, const int32_t* pa, int32_t n,
                   int32_t r, float* tar, float* van, void* ws, hipStream_t st, Between between = no_mark,
-                  int64_t zero_chunks = 0, bool adjacent = false) {
+                  int64_t zero_chunks = 0, bool adjacent = false, const double* cv_tau = nullptr) {
 #define IPV_SCORES(T, DD)                                                                                        \
   if (d.D == DD)                                                                                                 \
-    return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between, zero_chunks, adjacent);
+    return run_scores<T, DD>(d, K, V, fr, pa, n, r, tar, van, ws, st, between, zero_chunks, adjacent, cv_tau);
   if (d.dtype == IPV_BF16) {
     IPV_SCORES(uint16_t, 32) IPV_SCORES(uint16_t, 64) IPV_SCORES(uint16_t, 128) IPV_SCORES(uint16_t, 256)
   } else {
@@ -249,10 +260,12 @@ ipv_status scores(const Dims& d, const void* K, const void* V, const int32_t* fr
   return IPV_ERR_SHAPE;
 }
 
+// cv_done: the TaR launch has computed the windows already (k_tar_sweep_cv)
 ipv_status pool_d(const Dims& d, const double* tau, float* van, const int32_t* fr, const int32_t* pa, int32_t n,
-                  int32_t* pool_out, void* ws, hipStream_t st) {
-  k_pool_cv<<<dim3((uint32_t)(d.B * d.L)), dim3(kPoolThreads), 0, st>>>(van, d.S, n, (int32_t)d.H, tau[0], tau[1],
-                                                                        tau[2], ws_pool(ws, d), pool_out);
+                  int32_t* pool_out, void* ws, hipStream_t st, bool cv_done = false) {
+  if (!cv_done)
+    k_pool_cv<<<dim3((uint32_t)(d.B * d.L)), dim3(kPoolThreads), 0, st>>>(van, d.S, n, (int32_t)d.H, tau[0], tau[1],
+                                                                          tau[2], ws_pool(ws, d), pool_out);
   k_pool_apply<<<dim3((uint32_t)d.slices), dim3(kPoolThreads), 0, st>>>(
       van, fr, pa, d.S, n, (int32_t)d.H, d.gh, d.gw, ws_pool(ws, d), make_fastdiv((uint32_t)d.p),
       make_fastdiv((uint32_t)d.gw));
@@ -473,14 +486,17 @@ ipv_status compress_run(const Dims& d, void* K, void* V, int32_t* fr, int32_t* p
     return hipEventRecord(static_cast<hipEvent_t>(events->at[i]), st) == hipSuccess ? IPV_OK : IPV_ERR_HIP;
   };
   const bool uniform = (mode & IPV_UNIFORM_SELECT) != 0;  // no scores: frame ids decide
+  const bool adjacent = (mode & IPV_TAR_ADJACENT) != 0;
+  // with the recent-key table, the pooling CV runs in the TaR launch
+  const bool cv_fused = cv_tau && !uniform && !adjacent;
   IPV_TRY(mark(0));
   if (uniform)
     IPV_TRY(mark(1));
   else
     IPV_TRY(scores(d, K, V, fr, pa, n, r, tar, van, ws, st, [&]() { return mark(1); }, compact_chunks(budget),
-                   (mode & IPV_TAR_ADJACENT) != 0));
+                   adjacent, cv_fused ? cv_tau : nullptr));
   IPV_TRY(mark(2));
-  if (cv_tau && !uniform) IPV_TRY(pool_d(d, cv_tau, van, fr, pa, n, nullptr, ws, st));
+  if (cv_tau && !uniform) IPV_TRY(pool_d(d, cv_tau, van, fr, pa, n, nullptr, ws, st, cv_fused));
   IPV_TRY(mark(3));
   // the score launches zero the compaction's flags; without them the uniform selection does
   IPV_TRY(select(d, tar, van, fr, n, budget, floor_share(alpha, budget), r, keep, err_word(ws), st, mode,

@@ -413,18 +413,20 @@ __global__ __launch_bounds__(256) void k_table_van(const T* __restrict__ K, cons
 }
 
 // ---------------------------------------------------------------- adaptive pooling
-// Both kernels run kPoolThreads threads a workgroup; a thread takes rows
-// tid, tid + kPoolThreads, ... and issues kPoolBatch of their loads at once
-// (buffer loads: rows past n read as zero and are left out).
+// The pooling kernels run kPoolThreads threads a workgroup (the CV also runs
+// in 256-thread blocks beside the TaR tiles); a thread takes rows tid,
+// tid + threads, ... and issues kPoolBatch of their loads at once (buffer
+// loads: rows past n read as zero and are left out).
 constexpr int kPoolThreads = 1024;
 constexpr int kPoolBatch = 8;
 constexpr int kPoolHeads = 4;  // the CV loads this many heads' rows at once
 
-// Sum over the workgroup in a fixed order: a butterfly inside each wave, then
-// the wave totals in wave order. Every thread gets the sum. red: one slot per
-// wave, free again when this returns.
+// Sum over the NT threads of a workgroup in a fixed order: a butterfly inside
+// each wave, then the wave totals in wave order. Every thread gets the sum.
+// red: one slot per wave, free again when this returns.
+template <int NT>
 __device__ __forceinline__ double pool_block_sum(double v, double* red) {
-  constexpr int NW = kPoolThreads / kWave;
+  constexpr int NW = NT / kWave;
 #pragma unroll
   for (int off = kWave / 2; off >= 1; off /= 2) v += __shfl_xor(v, off);
   if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = v;
@@ -436,17 +438,15 @@ __device__ __forceinline__ double pool_block_sum(double v, double* red) {
   return t;
 }
 
-// Per (stream, layer): CV of all H * n VaN values in fp64, two passes (mean,
-// then squared deviations), each a fixed-order reduction; window k from the
-// thresholds. One workgroup per (stream, layer).
-__global__ __launch_bounds__(kPoolThreads) void k_pool_cv(const float* __restrict__ van, int64_t S, int32_t n,
-                                                          int32_t H, double tau1, double tau2, double tau3,
-                                                          int32_t* __restrict__ pool_ws,
-                                                          int32_t* __restrict__ pool_out) {
-  constexpr int NT = kPoolThreads, U = kPoolBatch;
-  __shared__ double red[NT / kWave];
-  const int tid = threadIdx.x;
-  const int64_t bl = blockIdx.x;
+// Per (stream, layer) bl: CV of all H * n VaN values in fp64, two passes
+// (mean, then squared deviations), each a fixed-order reduction; window k
+// from the thresholds, written to pool_ws[bl] (and pool_out[bl] if given).
+// NT threads (tid in [0, NT)); red: NT / 64 doubles of LDS.
+template <int NT>
+__device__ __forceinline__ void pool_cv_block(const float* __restrict__ van, int64_t S, int32_t n, int32_t H,
+                                              double tau1, double tau2, double tau3, int32_t* __restrict__ pool_ws,
+                                              int32_t* __restrict__ pool_out, int64_t bl, int tid, double* red) {
+  constexpr int U = kPoolBatch;
   const double count = (double)H * (double)n;
   // Pass `second`: the sum of the values, else of their squared deviations
   // from `mean`. Loads go out kPoolHeads heads x kPoolBatch rows at a time
@@ -477,15 +477,24 @@ __global__ __launch_bounds__(kPoolThreads) void k_pool_cv(const float* __restric
     }
     return acc;
   };
-  const double mean = pool_block_sum(sweep(false, 0.0), red) / count;
+  const double mean = pool_block_sum<NT>(sweep(false, 0.0), red) / count;
   const double v = sweep(true, mean);
-  const double sd = sqrt(pool_block_sum(v, red) / count);
+  const double sd = sqrt(pool_block_sum<NT>(v, red) / count);
   if (tid == 0) {
     const double cv = mean == 0.0 ? 0.0 : sd / mean;
     const int32_t k = cv < tau1 ? 7 : cv < tau2 ? 5 : cv < tau3 ? 3 : 1;
     pool_ws[bl] = k;
     if (pool_out) pool_out[bl] = k;
   }
+}
+
+// One workgroup per (stream, layer).
+__global__ __launch_bounds__(kPoolThreads) void k_pool_cv(const float* __restrict__ van, int64_t S, int32_t n,
+                                                          int32_t H, double tau1, double tau2, double tau3,
+                                                          int32_t* __restrict__ pool_ws,
+                                                          int32_t* __restrict__ pool_out) {
+  __shared__ double red[kPoolThreads / kWave];
+  pool_cv_block<kPoolThreads>(van, S, n, H, tau1, tau2, tau3, pool_ws, pool_out, blockIdx.x, threadIdx.x, red);
 }
 
 // The k x k window mean is separable: every cell first gets the sum and count
@@ -660,6 +669,40 @@ __global__ __launch_bounds__(kPoolThreads) void k_pool_apply(float* __restrict__
       }
     }
   }
+}
+
+// ---------------------------------------------------------------- TaR tiles with the pooling CV
+// The TaR half of the sweep with the CV of the layer-adaptive pooling beside
+// it (the VaN scores are final after the previous launch): blocks
+// [0, cv_padded) compute the CV of (stream, layer) blockIdx.x (those at or
+// past cv_real return at once), the rest are TaR tiles as in k_score_sweep.
+// cv_padded is a multiple of 8, so tile block i + cv_padded runs on XCD i % 8.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_tar_sweep_cv(const T* __restrict__ K, const int32_t* __restrict__ patch_idx,
+                                                      int64_t S, int32_t n, int32_t p, const float* __restrict__ table,
+                                                      const int32_t* __restrict__ first_recent,
+                                                      float* __restrict__ tar, uint32_t* err, TileGrid g,
+                                                      int32_t sure_past, const float* __restrict__ van, int32_t H,
+                                                      double tau1, double tau2, double tau3,
+                                                      int32_t* __restrict__ pool_ws, uint32_t cv_padded,
+                                                      uint32_t cv_real) {
+  __shared__ double red[256 / kWave];
+  if (blockIdx.x < cv_padded) {
+    if (blockIdx.x < cv_real)
+      pool_cv_block<256>(van, S, n, H, tau1, tau2, tau3, pool_ws, nullptr, blockIdx.x, threadIdx.x, red);
+    return;
+  }
+  using C = SweepCfg<T, D>;
+  const uint32_t logical = xcd_logical_id(blockIdx.x - cv_padded, g.blocks);
+  if (logical >= g.n_work) return;
+  const uint32_t tile = fast_div(logical, g.col_blocks);
+  const uint32_t colblock = logical - tile * g.col_blocks.d;
+  const uint32_t slice = fast_div(tile, g.frame_blocks);
+  const uint32_t f0 = (tile - slice * g.frame_blocks.d) * C::U;
+  const bool tail = (int64_t)(f0 + C::U) * p > sure_past;
+  const uint32_t rec = tail ? (uint32_t)first_recent[slice] : (uint32_t)n;
+  sweep_tile<T, D, true, false>(K, nullptr, patch_idx, S, n, p, table, rec, tar, nullptr, err, slice, f0, colblock,
+                                threadIdx.x);
 }
 
 }  // namespace ipv
