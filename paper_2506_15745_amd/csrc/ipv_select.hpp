@@ -202,12 +202,13 @@ __device__ __forceinline__ void block_min_max(const uint32_t (&key)[RPT], uint64
 }
 
 // Rows [row0, row0 + RPT) of one slice's column (S rows of 4 bytes); rows at
-// or past S read as 0. VEC: rows are 16-byte aligned (S % 4 == 0), so a run
-// lies wholly inside or wholly past the column and loads 16 bytes at a time.
+// or past S read as 0, and so does every row when `present` is false (an
+// empty resource). VEC: rows are 16-byte aligned (S % 4 == 0), so a run lies
+// wholly inside or wholly past the column and loads 16 bytes at a time.
 template <int RPT, bool VEC>
 __device__ __forceinline__ void load_row_run(const void* __restrict__ col, int64_t S, int64_t row0,
-                                             uint32_t (&out)[RPT]) {
-  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(col, (uint32_t)(S * 4));
+                                             uint32_t (&out)[RPT], bool present = true) {
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(col, present ? (uint32_t)(S * 4) : 0u);
   if (VEC) {
 #pragma unroll
     for (int i = 0; i < RPT; i += 4) {
@@ -223,22 +224,32 @@ __device__ __forceinline__ void load_row_run(const void* __restrict__ col, int64
   }
 }
 
+// Heads after the first whose runs are loaded together (the rest of a
+// layer's heads in one round trip when a thread holds few rows).
+template <int RPT>
+constexpr int head_batch() { return RPT <= 8 ? 3 : 1; }
+
 // A score run summed over `heads` consecutive slices (column stride S) in
 // fp32, head 0 first, starting from +0 (the order the keep decision is
-// defined in); heads == 1 is the slice's own run.
+// defined in); heads == 1 is the slice's own run. Absent heads of a batch
+// read as +0, which leaves every sum unchanged.
 template <int RPT, bool VEC>
 __device__ __forceinline__ void load_score_run(const float* __restrict__ col, int64_t S, int32_t heads, int64_t row0,
                                                uint32_t (&out)[RPT]) {
+  constexpr int G = head_batch<RPT>();
   load_row_run<RPT, VEC>(col, S, row0, out);
   if (heads == 1) return;
 #pragma unroll
   for (int i = 0; i < RPT; ++i) out[i] = __float_as_uint(0.f + __uint_as_float(out[i]));
 #pragma unroll 1
-  for (int32_t h = 1; h < heads; ++h) {
-    uint32_t t[RPT];
-    load_row_run<RPT, VEC>(col + h * S, S, row0, t);
+  for (int32_t h = 1; h < heads; h += G) {
+    uint32_t t[G][RPT];
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) out[i] = __float_as_uint(__uint_as_float(out[i]) + __uint_as_float(t[i]));
+    for (int g = 0; g < G; ++g) load_row_run<RPT, VEC>(col + min(h + g, heads - 1) * S, S, row0, t[g], h + g < heads);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) out[i] = __float_as_uint(__uint_as_float(out[i]) + __uint_as_float(t[g][i]));
   }
 }
 
@@ -247,13 +258,17 @@ __device__ __forceinline__ void load_score_run(const float* __restrict__ col, in
 template <int RPT, bool VEC>
 __device__ __forceinline__ bool heads_differ(const int32_t* __restrict__ fr0, int64_t S, int32_t heads, int64_t row0,
                                              int32_t n, const uint32_t (&fr)[RPT]) {
+  constexpr int G = head_batch<RPT>();
   bool diff = false;
 #pragma unroll 1
-  for (int32_t h = 1; h < heads; ++h) {
-    uint32_t t[RPT];
-    load_row_run<RPT, VEC>(fr0 + h * S, S, row0, t);
+  for (int32_t h = 1; h < heads; h += G) {
+    uint32_t t[G][RPT];
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) diff |= row0 + i < n && t[i] != fr[i];
+    for (int g = 0; g < G; ++g) load_row_run<RPT, VEC>(fr0 + min(h + g, heads - 1) * S, S, row0, t[g], h + g < heads);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) diff |= h + g < heads && row0 + i < n && t[g][i] != fr[i];
   }
   return diff;
 }
