@@ -38,9 +38,8 @@
 //     l % kHistCopies, so lanes of one wave that hit the same bin mostly hit
 //     different words in different banks;
 //   * scans take one barrier: each wave adds up the wave totals it needs;
-//   * the keep set is gathered in LDS in output order, then written with
-//     consecutive stores (up to kStageRows rows; larger budgets store from
-//     the threads that own the rows).
+//   * the keep set is gathered in LDS in output order, kStageRows positions
+//     at a time, then written with consecutive stores.
 #pragma once
 
 #include "ipv_device.hpp"
@@ -54,7 +53,7 @@ constexpr int kHistCopies = 4;
 constexpr int kHistSkew = 4;
 constexpr int kHistStride = 256 + kHistSkew;
 constexpr int kHistWords = kHistCopies * kHistStride;
-constexpr int kStageRows = 8192;  // keep sets up to this size are gathered in LDS before the stores
+constexpr int kStageRows = 8192;  // keep-set positions gathered in LDS per round of stores
 
 template <int NT>
 struct SelShared {
@@ -275,22 +274,25 @@ __device__ __forceinline__ bool heads_differ(const int32_t* __restrict__ fr0, in
 
 // Writes the keep set: `kept` marks this thread's kept rows among its RPT
 // rows from row0, `pos` is the number of kept rows before them. `put(j, row)`
-// stores output position j. Sets of up to kStageRows rows are gathered in LDS
-// first, so that the global stores are consecutive across the block.
+// stores output position j. The set is gathered in LDS in output order,
+// kStageRows positions at a time, so that the global stores are consecutive
+// across the block.
 template <int NT, int RPT, typename Put>
 __device__ __forceinline__ void write_keep(uint64_t kept, int32_t pos, int32_t budget, int64_t row0,
                                            SelShared<NT>& sh, Put put) {
-  if (budget > kStageRows) {
+  for (int32_t lo = 0; lo < budget; lo += kStageRows) {
+    const int32_t hi = min(budget, lo + kStageRows);
+    int32_t q = pos;
 #pragma unroll
     for (int i = 0; i < RPT; ++i)
-      if (((kept >> i) & 1ull) && pos < budget) put(pos++, (int32_t)(row0 + i));
-    return;
+      if (((kept >> i) & 1ull) && q < budget) {
+        if (q >= lo && q < hi) sh.stage[q - lo] = (int32_t)(row0 + i);
+        ++q;
+      }
+    __syncthreads();
+    for (int32_t j = threadIdx.x; j < hi - lo; j += (int32_t)blockDim.x) put(lo + j, sh.stage[j]);
+    if (hi < budget) __syncthreads();  // the next positions reuse the stage
   }
-#pragma unroll
-  for (int i = 0; i < RPT; ++i)
-    if (((kept >> i) & 1ull) && pos < budget) sh.stage[pos++] = (int32_t)(row0 + i);
-  __syncthreads();
-  for (int32_t j = threadIdx.x; j < budget; j += (int32_t)blockDim.x) put(j, sh.stage[j]);
 }
 
 // One group of `heads` slices (1: a slice of its own) with NT threads. VEC:
