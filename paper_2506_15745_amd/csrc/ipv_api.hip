@@ -278,6 +278,7 @@ __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t v) {
 }
 
 constexpr int kSelThreads = 1024;  // most threads of a selection workgroup
+constexpr int64_t kComputeUnits = 256;  // MI355X
 
 // Threads of a selection workgroup: whole waves for the n rows at RPT rows a
 // thread, at most kSelThreads (the caller picks RPT >= n / kSelThreads).
@@ -334,6 +335,13 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
     if (rpt <= 32) return run_uniform<32>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
     return run_uniform<64>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
   }
+  // A block of up to 8 rows a thread (832 threads for 6272 rows) holds a CU
+  // alone; with more blocks than CUs, 16 rows a thread (half the threads)
+  // lets three blocks share a CU, which ends sooner although each block takes
+  // longer (16-stream 7B-class batch: 65 against 93 us).
+  const int64_t groups = d.slices / ((mode & IPV_HEAD_SHARED) ? d.H : 1);
+  if (groups > kComputeUnits && rpt <= 8)
+    return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
