@@ -328,20 +328,21 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
                   int32_t tar_total, int32_t r, int32_t* keep, uint32_t* err, hipStream_t st, uint32_t mode,
                   uint32_t* zero = nullptr, int32_t zero_per_slice = 0) {
   const int32_t rpt = (n + kSelThreads - 1) / kSelThreads;
+  // A block of up to 8 rows a thread (832 threads for 6272 rows) holds a CU
+  // alone; with more blocks than CUs, 16 rows a thread (half the threads)
+  // lets three blocks share a CU, which ends sooner although each block takes
+  // longer (16-stream 7B-class batch: 65 against 93 us).
+  const int64_t groups = d.slices / ((mode & IPV_HEAD_SHARED) ? d.H : 1);
+  const bool many = groups > kComputeUnits && rpt <= 8;
   if (mode & IPV_UNIFORM_SELECT) {
+    if (many) return run_uniform<16>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
     if (rpt <= 4) return run_uniform<4>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
     if (rpt <= 8) return run_uniform<8>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
     if (rpt <= 16) return run_uniform<16>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
     if (rpt <= 32) return run_uniform<32>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
     return run_uniform<64>(d, fr, n, budget, r, keep, err, st, mode, zero, zero_per_slice);
   }
-  // A block of up to 8 rows a thread (832 threads for 6272 rows) holds a CU
-  // alone; with more blocks than CUs, 16 rows a thread (half the threads)
-  // lets three blocks share a CU, which ends sooner although each block takes
-  // longer (16-stream 7B-class batch: 65 against 93 us).
-  const int64_t groups = d.slices / ((mode & IPV_HEAD_SHARED) ? d.H : 1);
-  if (groups > kComputeUnits && rpt <= 8)
-    return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
+  if (many) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);

@@ -9,6 +9,7 @@ import torch
 import oracle
 import synth
 from synth import workloads as W
+from paper_2506_15745_amd import ipv
 from tests import parity as P
 
 pytestmark = pytest.mark.gpu
@@ -279,3 +280,23 @@ def test_compaction_at_chunk_boundaries(C):
     assert np.array_equal(Kh[..., :C, :], K[..., keep1, :]) and np.array_equal(Vh[..., :C, :], V[..., keep1, :])
     assert np.array_equal(fh[..., :C], fr[..., keep1]) and np.array_equal(ph[..., :C], pa[..., keep1])
     assert np.array_equal(Kh[..., n:, :], K[..., n:, :])
+
+
+@pytest.mark.parametrize("mode", [0, ipv.UNIFORM_SELECT, ipv.TAR_REVERSE | ipv.VAN_REVERSE])
+def test_more_slices_than_compute_units(mode):
+    # 320 slices of few rows: the selection takes 16 rows a thread so that
+    # several of its blocks share a CU
+    L, H, D, gh, gw, r = 80, 4, 32, 14, 14, 2
+    n = 8 * gh * gw
+    st = synth.fresh_cache(61, L, H, n, D, gh, gw, n, synth.BF16, synth.RhoSpec(0.0, 0.99), (0.5,))
+    K, V, fr, pa = (np.ascontiguousarray(getattr(st, a)[None]) for a in ("K", "V", "frame_idx", "patch_idx"))
+    budget = n // 2
+    Kd, Vd, frd, pad = P.to_device(K, "bf16"), P.to_device(V, "bf16"), P.to_device(fr), P.to_device(pa)
+    comp = ipv.Compressor(Kd, gh, gw, budget)
+    comp.compress(Kd, Vd, frd, pad, n, 0.5, r, mode=mode)
+    torch.cuda.synchronize()
+    assert comp.device_errors() == 0
+    got = P.GpuPass(P.to_host(comp.tar), P.to_host(comp.van), P.to_host(comp.keep_idx), P.to_host(Kd), P.to_host(Vd),
+                    P.to_host(frd), P.to_host(pad), 0)
+    near = P.check_pass("320 slices mode %d" % mode, K, V, fr, pa, n, budget, 0.5, r, gh, gw, mode, got)
+    print("  near-threshold rows %d" % near, flush=True)
