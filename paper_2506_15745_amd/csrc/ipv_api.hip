@@ -345,6 +345,7 @@ ipv_status select(const Dims& d, const float* tar, const float* van, const int32
   if (many) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 4) return run_select<4>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 8) return run_select<8>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
+  if (rpt <= 12) return run_select<12>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 16) return run_select<16>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   if (rpt <= 32) return run_select<32>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
   return run_select<64>(d, tar, van, fr, n, budget, tar_total, r, keep, err, st, mode);
