@@ -541,12 +541,13 @@ __device__ __forceinline__ float window_col(const float* hsum, const uint8_t* hc
 // One workgroup per slice. Frames are handled FR at a time: their raw VaN
 // values are scattered into an LDS grid (absent cells hold -1), then every
 // row of those frames averages the present cells of its k x k window (the
-// separable sums above) and overwrites its own score. Rows of later frames still hold raw values. Each
-// round starts at the smallest frame id not yet covered, so the loop runs at
-// most once per present frame whatever the ids are. Rows whose patch id is
-// outside the grid keep their raw value. A thread's first kPoolBatch rows
-// (all of them when n <= kPoolThreads * kPoolBatch) are loaded once and kept
-// in registers for every pass; later rows are loaded again in each pass.
+// separable sums above) and overwrites its own score. Rows of later frames
+// still hold raw values. Each round starts at the smallest frame id not yet
+// covered, so the loop runs at most once per present frame whatever the ids
+// are. Rows whose patch id is outside the grid keep their raw value. A
+// thread's first kPoolBatch rows (all of them when n <= kPoolThreads *
+// kPoolBatch) are loaded once and kept in registers for every pass; later
+// rows are loaded again in each pass.
 constexpr int kPoolCells = 8192;
 
 __global__ __launch_bounds__(kPoolThreads) void k_pool_apply(float* __restrict__ van,
